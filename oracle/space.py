@@ -1,0 +1,282 @@
+"""Reference schedule lattice (test infrastructure only).
+
+Definition 1 of the paper: a sketch fixes a sequence of transformations; an
+annotation assigns a value to each of its parameters; the kernel search space
+of a sketch is the set of every *valid* annotation.  Section 2.2 (Example 3)
+arranges those parameters as coordinates, one axis per varying parameter, and
+defines the neighbours of a point as the points one step away along a single
+axis.  This module is a plain restatement of the lattice the HIP library
+exposes; the C++ side is written separately and must agree with it bit for
+bit on every integer it produces.
+
+The paper's rule figures (sketch, initialisation, mutation) are missing, so the
+two lattices below are readings:
+
+conv2d (op 1), shape (N, C, H, W, K, R, S, stride, pad), axes in order
+    tk, th, tw, tc in {1, 2, 4, ..., 64}: output-tile extent along K, P, Q and
+        the input-channel chunk of one reduction step; kept if <= K, P, Q, C
+        (the smallest value is always kept);
+    unroll in {0, 16, 64, 512}: maximum unrolled steps of the reduction loop;
+    lds in {0, 1}: stage input and weight tiles in LDS;
+    ks in {1, 2, 4, 8}: reduction split over C across workgroups (kept if <= C);
+    mfma in {0, 1}: contract on fp32 MFMA (implicit GEMM) instead of VALU FMA.
+
+matmul (op 2), shape (M, N, K), axes in order
+    bm, bn in {16, 32, 64, 128, 256}: workgroup tile, kept if <= M, N;
+    bk in {4, 8, 16, 32, 64}: K-step of one LDS stage, kept if <= K;
+    unroll in {0, 16, 64, 512};  dbuf in {0, 1}: LDS double buffer;
+    mfma in {0, 1};  ks in {1, 2, 4, 8}: split-K across workgroups (kept if <= K).
+
+Validity is the hardware and register budget of the kernel family: at most
+1024 threads and 163840 bytes of LDS per workgroup, an accumulator budget per
+lane, MFMA tile minima, at most 2**31 - 1 workgroups, and a split no finer
+than the number of reduction steps.
+
+Pins: the neighbourhood reproduces Example 3 of Section 2.2
+(tests/golden/droplet_example3.txt); value lists, counts and hand-computed
+geometry of named points are checked in tests/test_oracle_space.py.
+"""
+from __future__ import annotations
+
+import math
+
+OP_CONV = 1
+OP_MATMUL = 2
+
+LDS_LIMIT = 163840
+THREADS_LIMIT = 1024
+GRID_LIMIT = 2 ** 31 - 1
+
+POW2_64 = [1, 2, 4, 8, 16, 32, 64]
+UNROLL = [0, 16, 64, 512]
+SPLITK = [1, 2, 4, 8]
+MM_TILE = [16, 32, 64, 128, 256]
+MM_BK = [4, 8, 16, 32, 64]
+
+CONV_AXES = ["tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma"]
+MM_AXES = ["bm", "bn", "bk", "unroll", "dbuf", "mfma", "ks"]
+
+
+def _clip(values, extent):
+    kept = [v for v in values if v <= extent]
+    return kept if kept else [min(values)]
+
+
+def _cdiv(a, b):
+    return -(-a // b)
+
+
+def _pow2floor(v):
+    p = 1
+    while p * 2 <= v:
+        p *= 2
+    return p
+
+
+def conv_out(shape):
+    N, C, H, W, K, R, S, st, pd = shape
+    return (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
+
+
+def check_shape(op, shape):
+    """Shapes the library accepts (raises ValueError otherwise)."""
+    if op == OP_CONV:
+        if len(shape) != 9:
+            raise ValueError("conv shape has 9 entries")
+        N, C, H, W, K, R, S, st, pd = shape
+        if N < 0 or min(C, H, W, K, R, S, st) < 1 or pd < 0:
+            raise ValueError("bad conv shape")
+        if H + 2 * pd < R or W + 2 * pd < S:
+            raise ValueError("conv shape has no output")
+    elif op == OP_MATMUL:
+        if len(shape) != 3:
+            raise ValueError("matmul shape has 3 entries")
+        M, N, K = shape
+        if M < 0 or N < 1 or K < 1:
+            raise ValueError("bad matmul shape")
+    else:
+        raise ValueError("unknown op")
+
+
+class Lattice:
+    """A product of ordered value lists with an optional validity predicate
+    (Definition 1: every valid annotation of one sketch)."""
+
+    def __init__(self, values, names=None, predicate=None):
+        self.values = [list(v) for v in values]
+        self.names = list(names) if names else [f"p{a}" for a in range(len(self.values))]
+        self.sizes = [len(v) for v in self.values]
+        self._pred = predicate
+
+    def size(self):
+        return math.prod(self.sizes)
+
+    def knobs(self, idx):
+        return {n: self.values[a][i] for a, (n, i) in enumerate(zip(self.names, idx))}
+
+    def key(self, idx):
+        """Mixed radix, axis 0 least significant."""
+        k, radix = 0, 1
+        for a, i in enumerate(idx):
+            k += i * radix
+            radix *= self.sizes[a]
+        return k
+
+    def from_key(self, key):
+        idx = []
+        for n in self.sizes:
+            idx.append(key % n)
+            key //= n
+        return tuple(idx)
+
+    def in_range(self, idx):
+        return len(idx) == len(self.sizes) and all(0 <= i < n for i, n in zip(idx, self.sizes))
+
+    def valid(self, idx):
+        if not self.in_range(idx):
+            return False
+        return True if self._pred is None else bool(self._pred(tuple(idx)))
+
+    def neighbors(self, idx):
+        """Example 3 of Section 2.2: one index step along one axis.  Axis order
+        ascending, the -1 step before the +1 step; out-of-range and invalid
+        points are left out."""
+        out = []
+        for a in range(len(self.sizes)):
+            for d in (-1, 1):
+                j = idx[a] + d
+                if 0 <= j < self.sizes[a]:
+                    nb = tuple(idx[:a]) + (j,) + tuple(idx[a + 1:])
+                    if self.valid(nb):
+                        out.append(nb)
+        return out
+
+    def origin(self):
+        """'Parameters that implement no optimization' (Section 2.2, step 1):
+        index 0 on every axis -- the smallest tile and chunk, no unrolling, no
+        LDS, no split, no MFMA.  If that point is invalid, the first valid
+        point in key order."""
+        z = tuple(0 for _ in self.sizes)
+        if self.valid(z):
+            return z
+        for k in range(self.size()):
+            p = self.from_key(k)
+            if self.valid(p):
+                return p
+        return None
+
+    def valid_points(self):
+        return [self.from_key(k) for k in range(self.size()) if self.valid(self.from_key(k))]
+
+
+class Space(Lattice):
+    """The lattice of one kernel family at one shape."""
+
+    def __init__(self, op, shape):
+        shape = tuple(int(v) for v in shape)
+        check_shape(op, shape)
+        self.op = op
+        self.shape = shape
+        if op == OP_CONV:
+            N, C, H, W, K, R, S, st, pd = shape
+            P, Q = conv_out(shape)
+            values = [
+                _clip(POW2_64, K), _clip(POW2_64, P), _clip(POW2_64, Q), _clip(POW2_64, C),
+                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1],
+            ]
+            names = CONV_AXES
+        else:
+            M, N, K = shape
+            values = [
+                _clip(MM_TILE, M), _clip(MM_TILE, N), _clip(MM_BK, K),
+                list(UNROLL), [0, 1], [0, 1], _clip(SPLITK, K),
+            ]
+            names = MM_AXES
+        super().__init__(values, names, predicate=lambda idx: self.geometry(idx)["valid"])
+
+    def geometry(self, idx):
+        """Launch geometry and derived template parameters; ``valid`` says
+        whether the point belongs to the search space."""
+        v = self.knobs(idx)
+        return conv_geometry(self.shape, v) if self.op == OP_CONV else matmul_geometry(self.shape, v)
+
+
+def conv_geometry(shape, v):
+    N, C, H, W, K, R, S, st, pd = shape
+    P, Q = conv_out(shape)
+    tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
+    npx = th * tw
+    if v["mfma"] == 0:
+        threads = min(256, _cdiv(npx, 64) * 64)
+        ppt = _cdiv(npx, threads)
+        acc = tk * ppt
+        body = acc
+        ok = acc <= 64
+        red = tc * R * S
+        t0, t1 = tk, ppt            # template parameters: TK, PPT
+    else:
+        threads = 256
+        ok = tk >= 16 and npx >= 64
+        tkb = max(1, tk // 16)
+        npb = max(1, npx // 64)
+        acc = 4 * tkb * npb
+        body = tkb * npb
+        ok = ok and acc <= 128
+        red = _cdiv(tc * R * S, 4) * 4
+        ppt = npb
+        t0, t1 = tkb, npb           # template parameters: 16-channel blocks, 16-pixel blocks per wave
+    hs = (th - 1) * st + R
+    ws = (tw - 1) * st + S
+    if v["lds"]:
+        lds = 4 * (tc * hs * ws + 1) + 4 * tk * red + 4 * red
+    else:
+        lds = 8 * red
+    chunks = max(1, _cdiv(C, tc))
+    grid = N * v["ks"] * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)
+    uf = 1 if v["unroll"] == 0 else min(16, _pow2floor(max(1, v["unroll"] // body)))
+    valid = (ok and lds <= LDS_LIMIT and threads <= THREADS_LIMIT and v["ks"] <= chunks
+             and grid <= GRID_LIMIT)
+    return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=acc,
+                unroll_eff=uf, t0=t0, t1=t1, red=red, chunks=chunks)
+
+
+def matmul_geometry(shape, v):
+    M, N, K = shape
+    bm, bn, bk = v["bm"], v["bn"], v["bk"]
+    if v["mfma"] == 0:
+        rm, rn = bm // 16, bn // 16
+        acc = rm * rn
+        body = acc
+        kstep = 1
+        ok = acc <= 128
+        t0, t1 = rm, rn
+    else:
+        ok = bm >= 32 and bn >= 32
+        wm, wn = bm // 2, bn // 2
+        if wm >= 32 and wn >= 32:
+            kstep = 2
+            blocks = (wm // 32) * (wn // 32)
+            acc = 16 * blocks
+        else:
+            kstep = 4
+            blocks = max(1, wm // 16) * max(1, wn // 16)
+            acc = 4 * blocks
+        body = blocks
+        ok = ok and acc <= 256
+        t0, t1 = wm, wn
+    trip = max(1, bk // kstep)
+    if v["unroll"] == 0:
+        uf = 1
+    elif trip * body <= v["unroll"]:
+        uf = trip
+    else:
+        uf = min(trip, _pow2floor(max(1, v["unroll"] // body)))
+    stages = 2 if v["dbuf"] else 1
+    lds = stages * (bm * (bk + 4) + bk * bn) * 4
+    nkt = _cdiv(K, bk)
+    grid = _cdiv(M, bm) * _cdiv(N, bn) * v["ks"]
+    threads = 256
+    valid = (ok and lds <= LDS_LIMIT and threads <= THREADS_LIMIT and v["ks"] <= nkt
+             and grid <= GRID_LIMIT)
+    return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=acc,
+                unroll_eff=uf, t0=t0, t1=t1, red=kstep, chunks=nkt)

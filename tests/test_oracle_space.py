@@ -1,0 +1,146 @@
+"""Pins of the reference lattice: the paper's worked neighbourhood example,
+hand-computed value lists and geometry, and structural invariants."""
+import math
+
+import pytest
+
+from oracle import space as sp
+
+
+def read_golden(path):
+    rows = {}
+    axes = []
+    for line in open(path):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        head, *rest = line.split()
+        if head == "axis":
+            axes.append([int(v) for v in rest[1:]])
+        else:
+            rows[head] = rest
+    return axes, rows
+
+
+def test_example3_neighbors(golden_dir):
+    axes, rows = read_golden(f"{golden_dir}/droplet_example3.txt")
+    lat = sp.Lattice(axes, ["unroll", "tile"])
+    point = tuple(axes[a].index(int(v)) for a, v in enumerate(rows["point"]))
+    got = [tuple(axes[a][i] for a, i in enumerate(nb)) for nb in lat.neighbors(point)]
+    expect = [tuple(int(t) for t in s.split(",")) for s in rows["neighbors"]]
+    assert got == expect
+    # (1,1) is a corner: two neighbours; the origin applies no optimisation.
+    assert lat.neighbors((0, 0)) == [(1, 0), (0, 1)]
+    assert lat.origin() == (0, 0)
+    assert lat.size() == 25
+
+
+def test_invalid_neighbors_skipped_not_hopped():
+    lat = sp.Lattice([[1, 2, 3], [1, 2, 4]], predicate=lambda p: p != (1, 1))
+    assert lat.neighbors((1, 0)) == [(0, 0), (2, 0)]
+    assert (1, 1) not in lat.valid_points() and len(lat.valid_points()) == 8
+    lat2 = sp.Lattice([[1, 2]], predicate=lambda p: p != (0,))
+    assert lat2.origin() == (1,)
+
+
+def test_key_mixed_radix():
+    lat = sp.Lattice([[0, 1, 2], [0, 1], [0, 1, 2, 3]])
+    assert lat.key((2, 1, 3)) == 2 + 1 * 3 + 3 * 6
+    keys = [lat.key(lat.from_key(k)) for k in range(lat.size())]
+    assert keys == list(range(24))
+
+
+def test_value_lists_named_shapes():
+    s0 = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
+    assert s0.values[0] == [1, 2, 4, 8, 16, 32, 64]
+    assert s0.values[1] == [1, 2, 4, 8, 16, 32] == s0.values[2]
+    assert s0.values[3] == [1, 2, 4, 8, 16, 32, 64]
+    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1]]
+    assert s0.size() == 7 * 6 * 6 * 7 * 4 * 2 * 4 * 2
+    s2 = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
+    assert s2.values[1] == [1, 2, 4, 8, 16, 32, 64]       # P = 112
+    assert s2.values[3] == [1, 2] and s2.values[6] == [1, 2]
+    m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
+    assert m.values == [[16, 32, 64, 128, 256]] * 2 + [[4, 8, 16, 32, 64], [0, 16, 64, 512],
+                                                         [0, 1], [0, 1], [1, 2, 4, 8]]
+    fc = sp.Space(sp.OP_MATMUL, (1, 1000, 2048))
+    assert fc.values[0] == [16]                          # smallest value kept
+    tiny = sp.Space(sp.OP_MATMUL, (3, 5, 2))
+    assert tiny.values[2] == [4] and tiny.values[6] == [1, 2]
+
+
+def idx_of(space, **kv):
+    return tuple(space.values[a].index(kv[n]) for a, n in enumerate(space.names))
+
+
+def test_conv_geometry_hand_computed():
+    s = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
+    g = s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1))
+    # 64 pixels -> one 16-pixel block per wave; 16 channels -> one block.
+    # reduction 16*9 = 144; halo 10x10; LDS 4*(16*100+1) + 4*16*144 + 4*144.
+    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256, lds_bytes=16196, acc=4,
+                     unroll_eff=16, t0=1, t1=1, red=144, chunks=4)
+    g = s.geometry(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0))
+    # 128 pixels -> 128 threads, 1 pixel each; acc 4; unroll 16//4 = 4.
+    assert g == dict(valid=True, grid=2 * 16 * 14 * 2, threads=128, lds_bytes=8 * 72, acc=4,
+                     unroll_eff=4, t0=4, t1=1, red=72, chunks=8)
+    # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
+    assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
+    # MFMA needs >= 16 channels and >= 64 pixels.
+    assert not s.valid(idx_of(s, tk=8, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
+    assert not s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
+    # LDS limit: 64-channel chunk of a 34x34 halo does not fit.
+    g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0))
+    assert g["lds_bytes"] == 4 * (64 * 34 * 34 + 1) + 4 * 16 * 576 + 4 * 576 and not g["valid"]
+    # split finer than the chunk count.
+    assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0))
+
+
+def test_matmul_geometry_hand_computed():
+    m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
+    g = m.geometry(idx_of(m, bm=64, bn=64, bk=16, unroll=64, dbuf=1, mfma=1, ks=1))
+    assert g == dict(valid=True, grid=256, threads=256, lds_bytes=2 * (64 * 20 + 16 * 64) * 4,
+                     acc=16, unroll_eff=8, t0=32, t1=32, red=2, chunks=64)
+    g = m.geometry(idx_of(m, bm=32, bn=128, bk=32, unroll=16, dbuf=0, mfma=1, ks=4))
+    # wave tile 16x64 -> 16x16x4 blocks: 1*4, acc 16; trip 8, 8*4 > 16 -> 16//4 = 4.
+    assert g == dict(valid=True, grid=32 * 8 * 4, threads=256, lds_bytes=(32 * 36 + 32 * 128) * 4,
+                     acc=16, unroll_eff=4, t0=16, t1=64, red=4, chunks=32)
+    g = m.geometry(idx_of(m, bm=128, bn=64, bk=8, unroll=512, dbuf=0, mfma=0, ks=1))
+    assert g == dict(valid=True, grid=8 * 16, threads=256, lds_bytes=(128 * 12 + 8 * 64) * 4,
+                     acc=32, unroll_eff=8, t0=8, t1=4, red=1, chunks=128)
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=0, ks=1))  # acc 256
+    assert m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=1, ks=1))      # AGPRs
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=64, unroll=0, dbuf=1, mfma=1, ks=1))  # LDS
+    assert not m.valid(idx_of(m, bm=16, bn=64, bk=8, unroll=0, dbuf=0, mfma=1, ks=1))    # MFMA min
+
+
+@pytest.mark.parametrize("op,shape", [
+    (sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1)),
+    (sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3)),
+    (sp.OP_MATMUL, (1024, 1024, 1024)),
+    (sp.OP_MATMUL, (1, 1000, 2048)),
+])
+def test_invariants(op, shape):
+    s = sp.Space(op, shape)
+    pts = s.valid_points()
+    assert pts and s.origin() == tuple(0 for _ in s.sizes)
+    for p in pts[:: max(1, len(pts) // 500)]:
+        g = s.geometry(p)
+        assert g["lds_bytes"] <= sp.LDS_LIMIT and g["threads"] <= 1024 and g["threads"] % 64 == 0
+        assert 1 <= g["unroll_eff"] <= 64 and g["grid"] >= 1
+        for nb in s.neighbors(p):
+            assert s.valid(nb) and sum(a != b for a, b in zip(nb, p)) == 1
+            assert sum(abs(a - b) for a, b in zip(nb, p)) == 1
+
+
+def test_shape_errors():
+    with pytest.raises(ValueError):
+        sp.Space(sp.OP_CONV, (1, 0, 4, 4, 1, 3, 3, 1, 1))
+    with pytest.raises(ValueError):
+        sp.Space(sp.OP_CONV, (1, 1, 2, 2, 1, 5, 5, 1, 0))
+    with pytest.raises(ValueError):
+        sp.Space(sp.OP_MATMUL, (4, 0, 4))
+    with pytest.raises(ValueError):
+        sp.Space(3, (4, 4, 4))
+    assert sp.Space(sp.OP_MATMUL, (0, 4, 4)).size() > 0     # empty output is a legal shape
+    assert math.prod(sp.Space(sp.OP_CONV, (0, 2, 4, 4, 2, 3, 3, 1, 1)).sizes) > 0
