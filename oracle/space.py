@@ -29,8 +29,9 @@ matmul (op 2), shape (M, N, K), axes in order
 
 Validity is the hardware and register budget of the kernel family: at most
 1024 threads and 163840 bytes of LDS per workgroup, an accumulator budget per
-lane, MFMA tile minima, at most 2**31 - 1 workgroups, and a split no finer
-than the number of reduction steps.
+lane, MFMA tile minima, a VALU conv tile of at least one wave (64 outputs), at
+most 2**31 - 1 workgroups, and a split no finer than the number of reduction
+steps.
 
 Pins: the neighbourhood reproduces Example 3 of Section 2.2
 (tests/golden/droplet_example3.txt); value lists, counts and hand-computed
@@ -206,15 +207,26 @@ def conv_geometry(shape, v):
     P, Q = conv_out(shape)
     tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
     npx = th * tw
+    outs = tk * npx
     if v["mfma"] == 0:
-        threads = min(256, _cdiv(npx, 64) * 64)
-        ppt = _cdiv(npx, threads)
-        acc = tk * ppt
+        # Lanes cover pixels first, then channel groups; a tile must fill at
+        # least one wave.
+        ok = outs >= 64
+        if npx >= 256:
+            threads, ppt, kpt = 256, npx // 256, tk
+        else:
+            threads = min(256, outs)
+            kpt = max(1, tk // max(1, threads // npx))
+            ppt = 1
+        acc = kpt * ppt
         body = acc
-        ok = acc <= 64
+        ok = ok and acc <= 64
         red = tc * R * S
-        t0, t1 = tk, ppt            # template parameters: TK, PPT
+        wrow = red
+        t0, t1 = kpt, ppt           # template parameters: channels and pixels per thread
     else:
+        # Four waves split the pixels; each wave covers all tk channels in
+        # 16x16 blocks (v_mfma_f32_16x16x4f32).
         threads = 256
         ok = tk >= 16 and npx >= 64
         tkb = max(1, tk // 16)
@@ -222,13 +234,13 @@ def conv_geometry(shape, v):
         acc = 4 * tkb * npb
         body = tkb * npb
         ok = ok and acc <= 128
-        red = _cdiv(tc * R * S, 4) * 4
-        ppt = npb
-        t0, t1 = tkb, npb           # template parameters: 16-channel blocks, 16-pixel blocks per wave
+        red = _cdiv(tc * R * S, 16) * 16
+        wrow = red + 4
+        t0, t1 = tkb, npb           # template parameters: channel blocks, pixel blocks per wave
     hs = (th - 1) * st + R
     ws = (tw - 1) * st + S
     if v["lds"]:
-        lds = 4 * (tc * hs * ws + 1) + 4 * tk * red + 4 * red
+        lds = 4 * (tc * hs * ws + 1) + 4 * tk * wrow + 4 * red
     else:
         lds = 8 * red
     chunks = max(1, _cdiv(C, tc))

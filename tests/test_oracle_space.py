@@ -78,12 +78,22 @@ def test_conv_geometry_hand_computed():
     g = s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1))
     # 64 pixels -> one 16-pixel block per wave; 16 channels -> one block.
     # reduction 16*9 = 144; halo 10x10; LDS 4*(16*100+1) + 4*16*144 + 4*144.
-    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256, lds_bytes=16196, acc=4,
+    # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148.
+    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256, lds_bytes=16452, acc=4,
                      unroll_eff=16, t0=1, t1=1, red=144, chunks=4)
     g = s.geometry(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0))
-    # 128 pixels -> 128 threads, 1 pixel each; acc 4; unroll 16//4 = 4.
-    assert g == dict(valid=True, grid=2 * 16 * 14 * 2, threads=128, lds_bytes=8 * 72, acc=4,
-                     unroll_eff=4, t0=4, t1=1, red=72, chunks=8)
+    # 128 pixels x 4 channels -> 256 threads, 2 channel groups of 2; unroll 16//2 = 8.
+    assert g == dict(valid=True, grid=2 * 16 * 14 * 2, threads=256, lds_bytes=8 * 72, acc=2,
+                     unroll_eff=8, t0=2, t1=1, red=72, chunks=8)
+    # One pixel, 64 channels: one wave, one channel per lane.
+    g = s.geometry(idx_of(s, tk=64, th=1, tw=1, tc=2, unroll=0, lds=1, ks=1, mfma=0))
+    assert g == dict(valid=True, grid=56 * 56, threads=64, lds_bytes=4 * (2 * 9 + 1) + 4 * 64 * 18
+                     + 4 * 18, acc=1, unroll_eff=1, t0=1, t1=1, red=18, chunks=32)
+    # Fewer than 64 outputs: not a full wave.
+    assert not s.valid(idx_of(s, tk=2, th=4, tw=4, tc=1, unroll=0, lds=0, ks=1, mfma=0))
+    # MFMA reduction padded to a multiple of 16: 4 channels x 9 taps = 36 -> 48.
+    g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1))
+    assert g["red"] == 48 and g["lds_bytes"] == 4 * (4 * 6 * 18 + 1) + 4 * 32 * 52 + 4 * 48
     # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
     assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
     # MFMA needs >= 16 channels and >= 64 pixels.
@@ -123,7 +133,9 @@ def test_matmul_geometry_hand_computed():
 def test_invariants(op, shape):
     s = sp.Space(op, shape)
     pts = s.valid_points()
-    assert pts and s.origin() == tuple(0 for _ in s.sizes)
+    assert pts and s.origin() == min(pts, key=s.key)
+    if op == sp.OP_MATMUL:
+        assert s.origin() == tuple(0 for _ in s.sizes)
     for p in pts[:: max(1, len(pts) // 500)]:
         g = s.geometry(p)
         assert g["lds_bytes"] <= sp.LDS_LIMIT and g["threads"] <= 1024 and g["threads"] % 64 == 0
