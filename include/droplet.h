@@ -1,0 +1,333 @@
+/*
+ * droplet.h -- C ABI of the MI355X (gfx950) schedule-tuning library.
+ *
+ * The library implements the hot path of the combined explore/exploit kernel
+ * scheduler of "Explore as a Storm, Exploit as a Raindrop" (Canesche, Verma,
+ * Pereira): a schedule-parameterised fp32 kernel family (NCHW conv2d and
+ * row-major matmul) written in HIP for gfx950, a hipEvent measurement harness,
+ * a seeded exploration sampler and Droplet Search coordinate descent.
+ *
+ * Conventions for every entry point:
+ *   - The return value is a status: DS_OK (0) or a negative DS_E* code.  No
+ *     C++ exception crosses the ABI.  ds_last_error() gives a thread-local
+ *     message for the last failing call on the calling thread.
+ *   - Device pointers are plain HIP device addresses owned by the caller
+ *     (allocated through PyTorch or hipMalloc), contiguous, 16-byte aligned.
+ *   - Streams are the caller's; work is enqueued asynchronously unless the
+ *     entry point says it synchronises.
+ *   - ds_sched is a plain value type owned by the caller; ds_space is opaque
+ *     and owned by the library until sched_space_destroy().
+ */
+#ifndef DROPLET_H
+#define DROPLET_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+    DS_OK = 0,
+    DS_EINVAL = -1,          /* bad argument (null pointer, bad shape, bad index) */
+    DS_EUNSUPPORTED = -2,    /* unknown op, or no device of the supported kind */
+    DS_EINVALID_SCHED = -3,  /* schedule outside the valid search space: nothing launched */
+    DS_EHIP = -4,            /* a HIP runtime call failed; see ds_last_error() */
+    DS_EPARITY = -5,         /* output failed the parity check against the reference */
+    DS_EBUDGET = -6,         /* Droplet stopped because its trial budget ran out (informational) */
+    DS_EEXHAUSTED = -7,      /* the lattice has no (more) valid point to draw */
+    DS_ENOMEM = -8           /* host or device allocation failed */
+};
+
+/* ---- operations -------------------------------------------------------- */
+enum {
+    DS_OP_CONV2D_NCHW = 1,   /* shape = {N,C,H,W,K,R,S,stride,pad}             */
+    DS_OP_MATMUL_RM = 2      /* shape = {M,N,K}                                */
+};
+
+#define DS_MAX_KNOBS 12
+#define DS_MAX_REPEATS 64
+
+/*
+ * A schedule: one point of the search space of a kernel family at a shape
+ * (Definition 1: an annotation of a sketch; Section 2.2: its coordinates).
+ * idx[a] is the position on axis a's ordered value list.  Entries of shape
+ * and idx beyond the op's length are ignored and should be zero.
+ */
+typedef struct {
+    int32_t op;
+    int32_t nknobs;
+    int64_t shape[9];
+    int32_t idx[DS_MAX_KNOBS];
+} ds_sched;
+
+typedef struct ds_space ds_space;
+
+/*
+ * sched_space_create -- the kernel search space of one kernel family at one
+ * shape (Definition 1).  conv2d axes, in order: tk, th, tw, tc (powers of two
+ * 1..64 kept if <= K, P, Q, C), unroll {0,16,64,512}, lds {0,1}, ks
+ * {1,2,4,8} (kept if <= C), mfma {0,1}.  matmul axes: bm, bn
+ * {16,...,256} (kept if <= M, N), bk {4,...,64} (kept if <= K), unroll,
+ * dbuf {0,1}, mfma {0,1}, ks {1,2,4,8} (kept if <= K).  The smallest value of
+ * a clipped axis is always kept.  Accepted shapes: conv N >= 0 (0 is the empty
+ * batch), C,H,W,K,R,S,stride >= 1, pad >= 0, at least one output position;
+ * matmul M >= 0, N,K >= 1.  *out receives a new space (free it with
+ * sched_space_destroy).  Errors: DS_EINVAL, DS_EUNSUPPORTED, DS_ENOMEM.
+ */
+int sched_space_create(int op, const int64_t *shape, int shape_len, ds_space **out);
+
+/*
+ * sched_space_create_lattice -- a generic lattice for exercising the search
+ * drivers with a caller-supplied cost (Section 2.2, Example 3 is such a
+ * lattice).  nvalues[a] values per axis, taken consecutively from values[].
+ * Every point is valid unless invalid_keys (nullable, n_invalid entries)
+ * lists its key.  The space has op 0 and cannot be launched.
+ */
+int sched_space_create_lattice(int nknobs, const int32_t *nvalues, const int32_t *values,
+                               const uint64_t *invalid_keys, int n_invalid, ds_space **out);
+
+void sched_space_destroy(ds_space *space);
+
+/* op, number of axes and number of lattice points (valid or not). */
+int sched_space_info(const ds_space *space, int *op, int *nknobs, uint64_t *size);
+
+/* Axis a: name (static string), number of values and the value list (owned
+ * by the space). */
+int sched_space_axis(const ds_space *space, int axis, const char **name, int *nvalues,
+                     const int32_t **values);
+
+/* 1 if s is a valid point of the space, 0 if not, < 0 on a bad argument. */
+int sched_valid(const ds_space *space, const ds_sched *s);
+
+/* Mixed-radix key: sum over axes of idx[a] * prod_{b<a} nvalues[b]. */
+int sched_key(const ds_space *space, const ds_sched *s, uint64_t *key);
+int sched_from_key(const ds_space *space, uint64_t key, ds_sched *out);
+
+/*
+ * sched_neighbors -- the neighbourhood of Section 2.2: points one index step
+ * away on one axis, axis order ascending, the -1 step before the +1 step;
+ * out-of-range and invalid points are left out.  Writes min(n, cap) points,
+ * *n_out = n (at most 2 * nknobs).
+ */
+int sched_neighbors(const ds_space *space, const ds_sched *s, ds_sched *out, int cap,
+                    int *n_out);
+
+/* The point that applies no optimisation (Section 2.2, step 1): index 0 on
+ * every axis, or the first valid point in key order.  DS_EEXHAUSTED if none. */
+int sched_origin(const ds_space *space, ds_sched *out);
+
+/* Launch geometry and derived template parameters of a point (valid or not). */
+typedef struct {
+    int32_t valid;
+    int32_t threads;      /* workgroup size */
+    int64_t grid;         /* number of workgroups (1-D) */
+    int32_t lds_bytes;    /* dynamic LDS per workgroup */
+    int32_t acc;          /* fp32 accumulators per lane */
+    int32_t unroll_eff;   /* unroll factor of the reduction loop */
+    int32_t t0, t1;       /* conv VALU: channels, pixels per thread; conv MFMA:
+                             16-channel blocks, 16-pixel blocks per wave;
+                             matmul VALU: rows, cols per thread; matmul MFMA:
+                             wave tile rows, cols */
+    int32_t red;          /* conv: reduction length per chunk; matmul: k per MFMA/FMA step */
+    int64_t chunks;       /* conv: reduction chunks; matmul: K-steps */
+} ds_geometry;
+int sched_geometry(const ds_space *space, const ds_sched *s, ds_geometry *out);
+
+/*
+ * ansor_draw -- the exploration sampler's draw sequence without measuring
+ * (Section 2.3, step 1; Section 2.1 annotation initialisation read as uniform
+ * draws): per draw, one index per axis from SplitMix64(seed), unbiased by
+ * rejection; invalid and repeated points are rejected; stops after n_explore
+ * distinct valid points or 100 * n_explore draws.  Writes *n_out points to out
+ * (capacity n_explore).
+ */
+int ansor_draw(const ds_space *space, uint64_t seed, int n_explore, ds_sched *out, int *n_out);
+
+/* 1 if a compiled kernel instance implements valid schedule s, 0 if not
+ * (host only, launches nothing). */
+int sched_has_kernel(const ds_space *space, const ds_sched *s);
+
+/* ---- kernels ------------------------------------------------------------ */
+
+/*
+ * kernel_run -- launch the kernel that schedule s selects (Definition 1: an
+ * annotated sketch is a concrete program).  conv: x = input [N,C,H,W], w =
+ * weight [K,C,R,S], y = output [N,K,P,Q] with P = (H+2pad-R)/stride+1 and
+ * Q likewise; y[n,k,p,q] = sum_{c,r,s} x[n,c,p*stride-pad+r,q*stride-pad+s] *
+ * w[k,c,r,s], out-of-range inputs read as 0.  matmul: x = A [M,K], w = B
+ * [K,N], y = C [M,N] = A*B, row-major.  fp32 in, out and accumulate.
+ * Asynchronous on stream; y is overwritten.  An empty output launches nothing.
+ * Errors: DS_EINVAL, DS_EINVALID_SCHED (nothing launched), DS_EHIP.
+ */
+int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float *y,
+               hipStream_t stream);
+
+/* The library's plain one-thread-per-output kernel for the same operation
+ * (used as the in-tuning reference when the caller supplies none). */
+int kernel_run_reference(int op, const int64_t *shape, const float *x, const float *w, float *y,
+                         hipStream_t stream);
+
+/* ---- measurement -------------------------------------------------------- */
+
+typedef struct {
+    int32_t warmup;        /* untimed launches before timing (default 3) */
+    int32_t repeat;        /* timed repeats (default 11, at most DS_MAX_REPEATS) */
+    double min_repeat_ms;  /* launches per repeat chosen so a repeat lasts this long (0.5) */
+    int32_t max_number;    /* cap on launches per repeat (200) */
+    double slow_cut;       /* a candidate whose first launch is slower than
+                              slow_cut * best_so_far is timed once only (4.0; 0 = never) */
+    double tol;            /* parity: max|y-ref| <= tol * max|ref| (1e-4) */
+    int32_t check;         /* 1: parity-check the first launch against ref */
+} ds_measure_cfg;
+
+/* Fills cfg with the defaults above. */
+void ds_measure_cfg_default(ds_measure_cfg *cfg);
+
+typedef struct {
+    int32_t status;        /* DS_OK, DS_EPARITY, DS_EHIP, DS_EINVALID_SCHED */
+    int32_t n_repeats;
+    int32_t number;        /* launches per repeat */
+    int32_t cut;           /* 1 if timed once because of slow_cut */
+    double median_ms;      /* median over repeats of (repeat time / number); +inf on failure */
+    double mean_ms;
+    double min_ms;
+    double first_ms;       /* time of the parity launch */
+    double max_err;        /* parity: max |y - ref| */
+    double max_ref;        /* parity: max |ref| */
+    int64_t nonfinite;     /* parity: count of non-finite outputs */
+    double repeats_ms[DS_MAX_REPEATS];
+} ds_measurement;
+
+/* Buffers a measurement runs on.  ref (nullable) is the fp32 reference output
+ * used by the parity check. */
+typedef struct {
+    const float *x;
+    const float *w;
+    float *y;
+    const float *ref;
+    hipStream_t stream;
+} ds_tune_io;
+
+/*
+ * ds_measure -- a5 of the hot path: parity-check the first launch (y is
+ * pre-filled with NaN; the check fails on NaN/Inf or max|y-ref| > tol*max|ref|),
+ * warm up, then time cfg->repeat repeats of `number` launches between two
+ * hipEvents on io->stream.  Synchronises the stream.  best_so_far_ms (0 = none)
+ * drives slow_cut.  out->status is the trial's status; the return value is
+ * DS_OK unless an argument is bad.
+ */
+int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cfg,
+               double best_so_far_ms, ds_measurement *out);
+
+/* Per-launch time of an empty kernel in the same harness (the dispatch floor). */
+int ds_empty_kernel_floor(hipStream_t stream, const ds_measure_cfg *cfg, ds_measurement *out);
+
+/* ---- tuning --------------------------------------------------------------- */
+
+/* A measurement callback: fills *out for schedule s, returns DS_OK or an error
+ * (an error is a failed trial with infinite time). */
+typedef int (*ds_measure_fn)(void *ctx, const ds_sched *s, ds_measurement *out);
+
+typedef struct {
+    int32_t n_explore;     /* exploration samples (300, Section 3 RQ1) */
+    int32_t budget;        /* Droplet trial cap (100, Section 3 RQ2) */
+    double alpha;          /* significance of "faster" (0.05; >= 1: plain median <) */
+    uint64_t seed;         /* sampler seed */
+    uint32_t frozen_mask;  /* bit a set: axis a is held at the start's value */
+    ds_measure_cfg measure;
+} ds_tune_cfg;
+
+void ds_tune_cfg_default(ds_tune_cfg *cfg);
+
+typedef struct {
+    ds_sched best;
+    double best_ms;
+    ds_sched seed_point;          /* best exploration sample (the Droplet start) */
+    double seed_ms;
+    int32_t status;               /* DS_OK, DS_EBUDGET (informational), DS_EEXHAUSTED, ... */
+    int32_t n_explore_measured;
+    int32_t n_droplet_measured;   /* new measurements made by Droplet (start included) */
+    int32_t n_failed;             /* failed trials (parity, launch) */
+    int32_t n_moves;              /* accepted Droplet moves */
+    double wall_s, explore_s, droplet_s;
+    ds_measurement best_meas;
+} ds_tune_result;
+
+typedef struct {
+    int32_t stage;                /* 0 explore, 1 droplet start, 2 droplet neighbour */
+    int32_t status;
+    uint64_t key;
+    double median_ms;
+} ds_trace_entry;
+
+typedef struct {
+    ds_trace_entry *entries;      /* caller-owned array of cap entries */
+    int32_t cap;
+    int32_t n;                    /* entries written (the library sets it) */
+} ds_trace;
+
+/*
+ * ansor_sample -- a2: draw n_explore points (as ansor_draw) and measure each
+ * on the GPU; *best is the fastest (ties: first drawn).  If io->ref is NULL
+ * the library computes a reference with kernel_run_reference.
+ */
+int ansor_sample(const ds_space *space, uint64_t seed, int n_explore, const ds_tune_io *io,
+                 const ds_measure_cfg *cfg, ds_sched *best, double *best_ms, ds_trace *trace);
+
+/*
+ * droplet_tune_ex -- a6: Droplet Search (Section 2.2) from start (NULL = the
+ * no-optimisation origin): measure the uncached valid neighbours of the
+ * current point, move to the fastest if it is faster (median lower and, for
+ * alpha < 1, one-sided rank-sum p < alpha, the 95% criterion of Section 3
+ * RQ4/RQ5), else stop.  At most `budget` neighbour measurements; the start is
+ * measured once more if needed.  fn NULL measures on the GPU with io (ref as in
+ * ansor_sample); otherwise fn(ctx, ...) supplies every measurement.
+ */
+int droplet_tune_ex(const ds_space *space, const ds_sched *start, int budget,
+                    const ds_tune_cfg *cfg, const ds_tune_io *io, ds_measure_fn fn, void *ctx,
+                    ds_tune_result *res, ds_trace *trace);
+
+/*
+ * ds_tune -- a7, the combined approach (Section 2.3): explore cfg->n_explore
+ * samples, give the best to Droplet Search with cfg->budget, run it to
+ * convergence.  Samples are cached, so Droplet never re-measures them.
+ */
+int ds_tune(const ds_space *space, const ds_tune_cfg *cfg, const ds_tune_io *io,
+            ds_measure_fn fn, void *ctx, ds_tune_result *res, ds_trace *trace);
+
+/*
+ * droplet_tune -- the four-argument form: builds the space, allocates seeded
+ * U[-1,1) inputs on the current device (SplitMix64 streams 240620037 for x / A
+ * and 240620038 for w, 240620039 for B), runs Droplet Search from start
+ * (NULL = origin) with `budget` on
+ * the default stream, frees everything, returns the best point and its median
+ * time in ms.
+ */
+int droplet_tune(int op, const int64_t *shape, const ds_sched *start, int budget, ds_sched *best,
+                 double *best_ms);
+
+/* ---- misc ------------------------------------------------------------------ */
+
+const char *ds_last_error(void);
+
+/* Host-side U[-1,1) SplitMix64 stream (the same definition the tests' input
+ * generator uses), for inputs the library creates itself. */
+int ds_gen_uniform(uint64_t seed, int64_t n, float *out);
+
+/* Current device: compute units, peak engine clock (kHz), arch name. */
+int ds_device_info(int *cus, int *clock_khz, char *arch, int arch_len);
+
+/* Number of compiled kernel instances (all families). */
+int ds_num_instances(void);
+
+/* Release library-owned device buffers of every device. */
+void ds_shutdown(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DROPLET_H */

@@ -29,8 +29,8 @@ matmul (op 2), shape (M, N, K), axes in order
 
 Validity is the hardware and register budget of the kernel family: at most
 1024 threads and 163840 bytes of LDS per workgroup, an accumulator budget per
-lane, MFMA tile minima, a VALU conv tile of at least one wave (64 outputs), at
-most 2**31 - 1 workgroups, and a split no finer than the number of reduction
+lane, MFMA tile minima, a VALU conv tile of at least one wave (64 outputs, or
+the largest tile of a smaller shape), at most 2**31 - 1 workgroups, and a split no finer than the number of reduction
 steps.
 
 Pins: the neighbourhood reproduces Example 3 of Section 2.2
@@ -210,8 +210,9 @@ def conv_geometry(shape, v):
     outs = tk * npx
     if v["mfma"] == 0:
         # Lanes cover pixels first, then channel groups; a tile must fill at
-        # least one wave.
-        ok = outs >= 64
+        # least one wave, or be the largest tile the shape allows.
+        biggest = _clip(POW2_64, K)[-1] * _clip(POW2_64, P)[-1] * _clip(POW2_64, Q)[-1]
+        ok = outs >= min(64, biggest)
         if npx >= 256:
             threads, ppt, kpt = 256, npx // 256, tk
         else:

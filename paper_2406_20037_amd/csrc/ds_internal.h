@@ -1,0 +1,129 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "droplet.h"
+
+namespace ds {
+
+// ---- errors ---------------------------------------------------------------
+void set_error(const char *fmt, ...);
+const char *last_error();
+
+// ---- lattice ----------------------------------------------------------------
+constexpr int kLdsLimit = 163840;     // bytes of LDS per workgroup on gfx950
+constexpr int kThreadsLimit = 1024;
+constexpr int64_t kGridLimit = 2147483647;
+
+struct Geometry {
+    bool valid = false;
+    int threads = 0;
+    int64_t grid = 0;
+    int lds_bytes = 0;
+    int acc = 0;
+    int unroll_eff = 1;
+    int t0 = 0, t1 = 0;
+    int red = 0;
+    int64_t chunks = 0;
+};
+
+struct Space {
+    int op = 0;                       // 0: generic lattice (no kernel)
+    int nknobs = 0;
+    int64_t shape[9] = {0};
+    std::vector<std::vector<int32_t>> values;
+    std::vector<const char *> names;
+    std::vector<uint64_t> invalid_keys;   // generic lattices only (sorted)
+    uint64_t size = 1;
+
+    bool in_range(const int32_t *idx) const;
+    uint64_t key(const int32_t *idx) const;
+    void from_key(uint64_t key, int32_t *idx) const;
+    Geometry geometry(const int32_t *idx) const;
+    bool valid(const int32_t *idx) const;
+    int value(const int32_t *idx, int axis) const { return values[axis][idx[axis]]; }
+};
+
+// Builds the space of a kernel family at a shape; returns DS_OK or an error.
+int build_space(int op, const int64_t *shape, int shape_len, Space &out);
+
+// Conv output extent.
+inline int64_t conv_out_dim(int64_t in, int64_t f, int64_t st, int64_t pd) {
+    return (in + 2 * pd - f) / st + 1;
+}
+
+ds_sched make_sched(const Space &sp, const int32_t *idx);
+bool sched_matches(const Space &sp, const ds_sched *s);
+
+// ---- launch plans -------------------------------------------------------------
+// Arguments of the conv kernels (passed by value).
+struct ConvArgs {
+    const float *x;
+    const float *w;
+    float *y;
+    int N, C, H, W, K, R, S, st, pd, P, Q;
+    int tk, th, tw, tc;
+    int tiles_k, tiles_p, tiles_q, ks;
+    int chunks, cps;      // reduction chunks, chunks per split
+    int red, wrow;        // reduction length per chunk, LDS weight row stride
+    int hs, ws;           // halo tile extent
+    int npx, npl;         // pixels per tile, lanes covering pixels (VALU)
+    int atomic;           // 1: accumulate into a zero-filled y
+};
+
+struct MatmulArgs {
+    const float *A;
+    const float *B;
+    float *C;
+    int M, N, K;
+    int tiles_m, tiles_n, ks;
+    int nkt, kps;         // K-tiles, K-tiles per split
+    int vecA, vecB;       // 1: 16-byte loads along K of A / along N of B are legal
+    int atomic;
+};
+
+struct Plan {
+    const void *func = nullptr;
+    int threads = 0;
+    int64_t grid = 0;
+    int lds = 0;
+    bool zero_fill = false;   // y must be zeroed first (split reduction)
+    int64_t y_elems = 0;
+    int op = 0;
+    ConvArgs conv{};
+    MatmulArgs mm{};
+};
+
+// Builds the plan of schedule s for buffers (x, w, y); DS_EINVALID_SCHED if s is
+// not a valid point.
+int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan &plan);
+int launch_plan(const Plan &plan, hipStream_t stream);
+
+// Kernel instance lookup (compiled template instances).
+const void *conv_valu_instance(int kpt, int ppt, int uf, int lds);
+const void *conv_mfma_instance(int tkb, int npb, int uf, int lds);
+const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf);
+const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf);
+int count_instances();
+
+// ---- measurement -----------------------------------------------------------------
+struct Meas {
+    int status = DS_OK;
+    double median = 0;
+    std::vector<double> repeats;
+    ds_measurement full{};
+};
+
+// Rank-sum test: one-sided p-value that a is stochastically smaller than b.
+double ranksum_p_less(const std::vector<double> &a, const std::vector<double> &b);
+bool better(const Meas &a, const Meas &b, double alpha);
+
+// Device helpers (harness).
+int fill_async(float *p, int64_t n, float v, hipStream_t stream);
+int reference_output(const Space &sp, const ds_tune_io *io, float **ref_out);
+void free_device(void *p);
+
+}  // namespace ds

@@ -1,0 +1,687 @@
+// Launch plans, kernel_run, reference kernels and the hipEvent measurement
+// harness (the "trial" of Section 2.1: observing one schedule's execution).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <mutex>
+#include <set>
+#include <utility>
+#include <vector>
+
+#include "kern_common.h"
+
+namespace ds {
+
+const void *g_conv_valu[kConvValuSlots];
+const void *g_conv_mfma[kConvMfmaSlots];
+const void *g_mm_valu[kMmValuSlots];
+const void *g_mm_mfma[kMmMfmaSlots];
+
+namespace {
+
+int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int log2_exact(int v) {
+    if (v < 1 || (v & (v - 1))) return -1;
+    int l = 0;
+    while ((1 << l) < v) ++l;
+    return l;
+}
+
+bool hip_ok(hipError_t e, const char *what) {
+    if (e == hipSuccess) return true;
+    set_error("%s: %s", what, hipGetErrorString(e));
+    return false;
+}
+
+// ---- small kernels ------------------------------------------------------------
+
+__global__ void fill_kernel(float *p, int64_t n, float v) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+__global__ void fill_u32_kernel(unsigned *p, int n) {
+    if (int(threadIdx.x) < n) p[threadIdx.x] = 0u;
+}
+
+// max |y - ref| and max |ref| (as order-preserving bit patterns of
+// non-negative floats) and the count of non-finite y.
+__global__ __launch_bounds__(256) void parity_kernel(const float *y, const float *ref, int64_t n,
+                                                     unsigned *out) {
+    float me = 0.f, mr = 0.f;
+    unsigned bad = 0;
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const float a = y[i], b = ref[i];
+        if (!isfinite(a)) bad++;
+        else me = fmaxf(me, fabsf(a - b));
+        mr = fmaxf(mr, fabsf(b));
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        me = fmaxf(me, __shfl_xor(me, off));
+        mr = fmaxf(mr, __shfl_xor(mr, off));
+        bad += __shfl_xor(bad, off);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        atomicMax(out + 0, __float_as_uint(me));
+        atomicMax(out + 1, __float_as_uint(mr));
+        atomicAdd(out + 2, bad);
+    }
+}
+
+__global__ void empty_kernel() {}
+
+// One thread per output, reduction in the definition's order (c, r, s / k).
+__global__ __launch_bounds__(256) void conv_ref_kernel(ConvArgs a) {
+    const int64_t total = int64_t(a.N) * a.K * a.P * a.Q;
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    int64_t f = i;
+    const int q = int(f % a.Q);
+    f /= a.Q;
+    const int p = int(f % a.P);
+    f /= a.P;
+    const int k = int(f % a.K);
+    const int n = int(f / a.K);
+    float acc = 0.f;
+    for (int c = 0; c < a.C; ++c)
+        for (int r = 0; r < a.R; ++r) {
+            const int iy = p * a.st - a.pd + r;
+            if (iy < 0 || iy >= a.H) continue;
+            for (int s = 0; s < a.S; ++s) {
+                const int ix = q * a.st - a.pd + s;
+                if (ix < 0 || ix >= a.W) continue;
+                acc = fmaf(a.x[((size_t(n) * a.C + c) * a.H + iy) * a.W + ix],
+                           a.w[((size_t(k) * a.C + c) * a.R + r) * a.S + s], acc);
+            }
+        }
+    a.y[i] = acc;
+}
+
+__global__ __launch_bounds__(256) void mm_ref_kernel(MatmulArgs a) {
+    const int64_t total = int64_t(a.M) * a.N;
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int m = int(i / a.N), nn = int(i % a.N);
+    float acc = 0.f;
+    for (int k = 0; k < a.K; ++k)
+        acc = fmaf(a.A[size_t(m) * a.K + k], a.B[size_t(k) * a.N + nn], acc);
+    a.C[i] = acc;
+}
+
+// ---- per-device state ------------------------------------------------------------
+
+constexpr int kMaxDevices = 64;
+std::mutex g_mu;
+unsigned *g_parity_buf[kMaxDevices];     // 4 words per device, library-owned
+std::set<std::pair<int, const void *>> g_lds_attr;
+
+int current_device(int &dev) {
+    if (!hip_ok(hipGetDevice(&dev), "hipGetDevice")) return DS_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("device index %d out of range", dev);
+        return DS_EUNSUPPORTED;
+    }
+    return DS_OK;
+}
+
+int parity_buffer(unsigned **out) {
+    int dev;
+    int rc = current_device(dev);
+    if (rc != DS_OK) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_parity_buf[dev]) {
+        void *p = nullptr;
+        if (!hip_ok(hipMalloc(&p, 16), "hipMalloc(parity)")) return DS_ENOMEM;
+        g_parity_buf[dev] = static_cast<unsigned *>(p);
+    }
+    *out = g_parity_buf[dev];
+    return DS_OK;
+}
+
+int ensure_lds_attr(const void *func, int lds) {
+    if (lds <= 65536) return DS_OK;
+    int dev;
+    int rc = current_device(dev);
+    if (rc != DS_OK) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_lds_attr.count({dev, func})) return DS_OK;
+    if (!hip_ok(hipFuncSetAttribute(func, hipFuncAttributeMaxDynamicSharedMemorySize, lds),
+                "hipFuncSetAttribute(MaxDynamicSharedMemorySize)"))
+        return DS_EHIP;
+    g_lds_attr.insert({dev, func});
+    return DS_OK;
+}
+
+void fill_conv_args(const Space &sp, const float *x, const float *w, float *y, ConvArgs &a) {
+    std::memset(&a, 0, sizeof a);
+    a.x = x;
+    a.w = w;
+    a.y = y;
+    a.N = int(sp.shape[0]);
+    a.C = int(sp.shape[1]);
+    a.H = int(sp.shape[2]);
+    a.W = int(sp.shape[3]);
+    a.K = int(sp.shape[4]);
+    a.R = int(sp.shape[5]);
+    a.S = int(sp.shape[6]);
+    a.st = int(sp.shape[7]);
+    a.pd = int(sp.shape[8]);
+    a.P = int(conv_out_dim(a.H, a.R, a.st, a.pd));
+    a.Q = int(conv_out_dim(a.W, a.S, a.st, a.pd));
+}
+
+void fill_mm_args(const Space &sp, const float *A, const float *B, float *C, MatmulArgs &a) {
+    std::memset(&a, 0, sizeof a);
+    a.A = A;
+    a.B = B;
+    a.C = C;
+    a.M = int(sp.shape[0]);
+    a.N = int(sp.shape[1]);
+    a.K = int(sp.shape[2]);
+}
+
+double elapsed_ms(hipEvent_t a, hipEvent_t b) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return std::numeric_limits<double>::quiet_NaN();
+    return double(ms);
+}
+
+struct Events {
+    std::vector<hipEvent_t> ev;
+    ~Events() {
+        for (auto e : ev) (void)hipEventDestroy(e);
+    }
+    bool make(int n) {
+        for (int i = 0; i < n; ++i) {
+            hipEvent_t e;
+            if (!hip_ok(hipEventCreate(&e), "hipEventCreate")) return false;
+            ev.push_back(e);
+        }
+        return true;
+    }
+};
+
+// Times `repeat` repeats of `number` launches of fn on stream.
+template <class F>
+int time_repeats(F &&fn, hipStream_t stream, int number, int repeat, double *rep) {
+    Events E;
+    if (!E.make(repeat + 1)) return DS_EHIP;
+    if (!hip_ok(hipEventRecord(E.ev[0], stream), "hipEventRecord")) return DS_EHIP;
+    for (int r = 0; r < repeat; ++r) {
+        for (int i = 0; i < number; ++i) {
+            const int rc = fn();
+            if (rc != DS_OK) return rc;
+        }
+        if (!hip_ok(hipEventRecord(E.ev[r + 1], stream), "hipEventRecord")) return DS_EHIP;
+    }
+    if (!hip_ok(hipEventSynchronize(E.ev[repeat]), "hipEventSynchronize")) return DS_EHIP;
+    for (int r = 0; r < repeat; ++r) rep[r] = elapsed_ms(E.ev[r], E.ev[r + 1]) / number;
+    return DS_OK;
+}
+
+void summarise(ds_measurement *out, int n) {
+    std::vector<double> v(out->repeats_ms, out->repeats_ms + n);
+    std::sort(v.begin(), v.end());
+    out->n_repeats = n;
+    out->median_ms = n % 2 ? v[n / 2] : 0.5 * (v[n / 2 - 1] + v[n / 2]);
+    out->min_ms = v.front();
+    double s = 0;
+    for (double t : v) s += t;
+    out->mean_ms = s / n;
+}
+
+}  // namespace
+
+// ---- instance lookup ---------------------------------------------------------------
+
+const void *conv_valu_instance(int kpt, int ppt, int uf, int lds) {
+    const int a = log2_exact(kpt), b = log2_exact(ppt), c = log2_exact(uf);
+    if (a < 0 || a > 6 || b < 0 || b > 4 || c < 0 || c > 4 || (lds & ~1)) return nullptr;
+    return g_conv_valu[((a * 5 + b) * 5 + c) * 2 + lds];
+}
+
+const void *conv_mfma_instance(int tkb, int npb, int uf, int lds) {
+    const int a = log2_exact(tkb), b = log2_exact(npb), c = log2_exact(uf);
+    if (a < 0 || a > 2 || b < 0 || b > 6 || c < 0 || c > 4 || (lds & ~1)) return nullptr;
+    return g_conv_mfma[((a * 7 + b) * 5 + c) * 2 + lds];
+}
+
+const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf) {
+    const int a = log2_exact(rm), b = log2_exact(rn), k = log2_exact(bk) - 2, c = log2_exact(uf);
+    if (a < 0 || a > 4 || b < 0 || b > 4 || k < 0 || k > 4 || c < 0 || c > 6 || (dbuf & ~1))
+        return nullptr;
+    return g_mm_valu[(((a * 5 + b) * 5 + k) * 7 + c) * 2 + dbuf];
+}
+
+const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf) {
+    const int a = log2_exact(wm) - 4, b = log2_exact(wn) - 4, k = log2_exact(bk) - 2,
+              c = log2_exact(uf);
+    if (a < 0 || a > 3 || b < 0 || b > 3 || k < 0 || k > 4 || c < 0 || c > 6 || (dbuf & ~1))
+        return nullptr;
+    return g_mm_mfma[(((a * 4 + b) * 5 + k) * 7 + c) * 2 + dbuf];
+}
+
+int count_instances() {
+    int n = 0;
+    for (auto p : g_conv_valu) n += p != nullptr;
+    for (auto p : g_conv_mfma) n += p != nullptr;
+    for (auto p : g_mm_valu) n += p != nullptr;
+    for (auto p : g_mm_mfma) n += p != nullptr;
+    return n;
+}
+
+// ---- plans -------------------------------------------------------------------------
+
+int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan &plan) {
+    if (!s) {
+        set_error("schedule is null");
+        return DS_EINVAL;
+    }
+    Space sp;
+    const int len = s->op == DS_OP_CONV2D_NCHW ? 9 : 3;
+    int rc = build_space(s->op, s->shape, len, sp);
+    if (rc != DS_OK) return rc;
+    if (s->nknobs != sp.nknobs || !sp.in_range(s->idx)) {
+        set_error("schedule index vector does not fit the space");
+        return DS_EINVAL;
+    }
+    const Geometry g = sp.geometry(s->idx);
+    if (!g.valid) {
+        set_error("schedule is not a valid point of its search space");
+        return DS_EINVALID_SCHED;
+    }
+    plan = Plan();
+    plan.op = s->op;
+    plan.threads = g.threads;
+    plan.grid = g.grid;
+    plan.lds = g.lds_bytes;
+    if (s->op == DS_OP_CONV2D_NCHW) {
+        ConvArgs &a = plan.conv;
+        fill_conv_args(sp, x, w, y, a);
+        a.tk = sp.value(s->idx, 0);
+        a.th = sp.value(s->idx, 1);
+        a.tw = sp.value(s->idx, 2);
+        a.tc = sp.value(s->idx, 3);
+        const int lds = sp.value(s->idx, 5);
+        a.ks = sp.value(s->idx, 6);
+        const int mfma = sp.value(s->idx, 7);
+        a.tiles_k = int(cdiv64(a.K, a.tk));
+        a.tiles_p = int(cdiv64(a.P, a.th));
+        a.tiles_q = int(cdiv64(a.Q, a.tw));
+        a.chunks = int(g.chunks);
+        a.cps = int(cdiv64(a.chunks, a.ks));
+        a.red = g.red;
+        a.wrow = mfma ? g.red + 4 : g.red;
+        a.hs = (a.th - 1) * a.st + a.R;
+        a.ws = (a.tw - 1) * a.st + a.S;
+        a.npx = a.th * a.tw;
+        a.npl = std::min(a.npx, 256);
+        a.atomic = a.ks > 1;
+        plan.func = mfma ? conv_mfma_instance(g.t0, g.t1, g.unroll_eff, lds)
+                         : conv_valu_instance(g.t0, g.t1, g.unroll_eff, lds);
+        plan.zero_fill = a.ks > 1;
+        plan.y_elems = int64_t(a.N) * a.K * a.P * a.Q;
+    } else {
+        MatmulArgs &a = plan.mm;
+        fill_mm_args(sp, x, w, y, a);
+        const int bm = sp.value(s->idx, 0), bn = sp.value(s->idx, 1), bk = sp.value(s->idx, 2);
+        const int dbuf = sp.value(s->idx, 4), mfma = sp.value(s->idx, 5);
+        a.ks = sp.value(s->idx, 6);
+        a.tiles_m = int(cdiv64(a.M, bm));
+        a.tiles_n = int(cdiv64(a.N, bn));
+        a.nkt = int(g.chunks);
+        a.kps = int(cdiv64(a.nkt, a.ks));
+        a.vecA = (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
+        a.vecB = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
+        a.atomic = a.ks > 1;
+        plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf)
+                         : mm_valu_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf);
+        plan.zero_fill = a.ks > 1;
+        plan.y_elems = int64_t(a.M) * a.N;
+    }
+    if (!plan.func) {
+        set_error("no compiled kernel instance for this schedule");
+        return DS_EUNSUPPORTED;
+    }
+    return DS_OK;
+}
+
+int fill_async(float *p, int64_t n, float v, hipStream_t stream) {
+    if (n <= 0) return DS_OK;
+    const int64_t blocks = std::min<int64_t>(cdiv64(n, 256), 4096);
+    hipLaunchKernelGGL(fill_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, p, n, v);
+    return hip_ok(hipGetLastError(), "fill launch") ? DS_OK : DS_EHIP;
+}
+
+int launch_plan(const Plan &plan, hipStream_t stream) {
+    if (plan.grid == 0 || plan.y_elems == 0) return DS_OK;
+    float *y = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.y : plan.mm.C;
+    if (plan.zero_fill) {
+        const int rc = fill_async(y, plan.y_elems, 0.f, stream);
+        if (rc != DS_OK) return rc;
+    }
+    int rc = ensure_lds_attr(plan.func, plan.lds);
+    if (rc != DS_OK) return rc;
+    void *args[1];
+    if (plan.op == DS_OP_CONV2D_NCHW) args[0] = const_cast<ConvArgs *>(&plan.conv);
+    else args[0] = const_cast<MatmulArgs *>(&plan.mm);
+    if (!hip_ok(hipLaunchKernel(plan.func, dim3(unsigned(plan.grid)), dim3(plan.threads), args,
+                                size_t(plan.lds), stream),
+                "hipLaunchKernel"))
+        return DS_EHIP;
+    return DS_OK;
+}
+
+int reference_output(const Space &sp, const ds_tune_io *io, float **ref_out) {
+    *ref_out = nullptr;
+    int64_t n;
+    if (sp.op == DS_OP_CONV2D_NCHW) {
+        const int64_t P = conv_out_dim(sp.shape[2], sp.shape[5], sp.shape[7], sp.shape[8]);
+        const int64_t Q = conv_out_dim(sp.shape[3], sp.shape[6], sp.shape[7], sp.shape[8]);
+        n = sp.shape[0] * sp.shape[4] * P * Q;
+    } else {
+        n = sp.shape[0] * sp.shape[1];
+    }
+    if (n == 0) return DS_OK;
+    void *p = nullptr;
+    if (!hip_ok(hipMalloc(&p, size_t(n) * sizeof(float)), "hipMalloc(reference)")) return DS_ENOMEM;
+    const int rc = kernel_run_reference(sp.op, sp.shape, io->x, io->w, static_cast<float *>(p),
+                                        io->stream);
+    if (rc != DS_OK || !hip_ok(hipStreamSynchronize(io->stream), "reference kernel")) {
+        (void)hipFree(p);
+        return rc != DS_OK ? rc : DS_EHIP;
+    }
+    *ref_out = static_cast<float *>(p);
+    return DS_OK;
+}
+
+void free_device(void *p) {
+    if (p) (void)hipFree(p);
+}
+
+}  // namespace ds
+
+using namespace ds;
+
+extern "C" {
+
+int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float *y,
+               hipStream_t stream) {
+    if (!s || s->op != op) {
+        set_error("schedule missing or for another op");
+        return DS_EINVAL;
+    }
+    Plan plan;
+    int rc = make_plan(s, x, w, y, plan);
+    if (rc != DS_OK) return rc;
+    if (plan.y_elems > 0 && plan.grid > 0 && (!x || !w || !y)) {
+        set_error("null buffer");
+        return DS_EINVAL;
+    }
+    return launch_plan(plan, stream);
+}
+
+int kernel_run_reference(int op, const int64_t *shape, const float *x, const float *w, float *y,
+                         hipStream_t stream) {
+    Space sp;
+    int rc = build_space(op, shape, op == DS_OP_CONV2D_NCHW ? 9 : 3, sp);
+    if (rc != DS_OK) return rc;
+    int64_t total;
+    if (op == DS_OP_CONV2D_NCHW) {
+        ConvArgs a;
+        fill_conv_args(sp, x, w, y, a);
+        total = int64_t(a.N) * a.K * a.P * a.Q;
+        if (total == 0) return DS_OK;
+        if (!x || !w || !y) {
+            set_error("null buffer");
+            return DS_EINVAL;
+        }
+        hipLaunchKernelGGL(conv_ref_kernel, dim3(unsigned(cdiv64(total, 256))), dim3(256), 0,
+                           stream, a);
+    } else {
+        MatmulArgs a;
+        fill_mm_args(sp, x, w, y, a);
+        total = int64_t(a.M) * a.N;
+        if (total == 0) return DS_OK;
+        if (!x || !w || !y) {
+            set_error("null buffer");
+            return DS_EINVAL;
+        }
+        hipLaunchKernelGGL(mm_ref_kernel, dim3(unsigned(cdiv64(total, 256))), dim3(256), 0,
+                           stream, a);
+    }
+    return hip_ok(hipGetLastError(), "reference launch") ? DS_OK : DS_EHIP;
+}
+
+int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cfg_in,
+               double best_so_far_ms, ds_measurement *out) {
+    if (!s || !io || !out) {
+        set_error("null argument");
+        return DS_EINVAL;
+    }
+    std::memset(out, 0, sizeof *out);
+    out->median_ms = out->mean_ms = out->min_ms = std::numeric_limits<double>::infinity();
+    ds_measure_cfg cfg;
+    if (cfg_in) cfg = *cfg_in;
+    else ds_measure_cfg_default(&cfg);
+    cfg.repeat = std::max(1, std::min(cfg.repeat, DS_MAX_REPEATS));
+    cfg.max_number = std::max(1, cfg.max_number);
+    cfg.warmup = std::max(0, cfg.warmup);
+
+    Plan plan;
+    int rc = make_plan(s, io->x, io->w, io->y, plan);
+    if (rc != DS_OK) {
+        out->status = rc;
+        return rc == DS_EINVALID_SCHED ? DS_OK : rc;
+    }
+    if (plan.y_elems > 0 && (!io->x || !io->w || !io->y)) {
+        set_error("null buffer");
+        return DS_EINVAL;
+    }
+    const hipStream_t stream = io->stream;
+    const bool check = cfg.check && io->ref && plan.y_elems > 0;
+    auto launch = [&]() { return launch_plan(plan, stream); };
+
+    // Parity launch on a NaN-filled output.
+    if (check) {
+        rc = fill_async(io->y, plan.y_elems, std::numeric_limits<float>::quiet_NaN(), stream);
+        if (rc != DS_OK) {
+            out->status = rc;
+            return DS_OK;
+        }
+    }
+    double first[1];
+    rc = time_repeats(launch, stream, 1, 1, first);
+    if (rc != DS_OK) {
+        out->status = rc;
+        return DS_OK;
+    }
+    out->first_ms = first[0];
+    if (check) {
+        unsigned *buf = nullptr;
+        rc = parity_buffer(&buf);
+        if (rc != DS_OK) {
+            out->status = rc;
+            return DS_OK;
+        }
+        hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, stream, buf, 4);
+        const int64_t blocks = std::min<int64_t>(cdiv64(plan.y_elems, 256), 1024);
+        hipLaunchKernelGGL(parity_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, io->y,
+                           io->ref, plan.y_elems, buf);
+        unsigned host[4] = {0, 0, 0, 0};
+        if (!hip_ok(hipGetLastError(), "parity launch") ||
+            !hip_ok(hipMemcpyAsync(host, buf, 16, hipMemcpyDeviceToHost, stream), "parity copy") ||
+            !hip_ok(hipStreamSynchronize(stream), "parity sync")) {
+            out->status = DS_EHIP;
+            return DS_OK;
+        }
+        float fe, fr;
+        std::memcpy(&fe, &host[0], 4);
+        std::memcpy(&fr, &host[1], 4);
+        out->max_err = fe;
+        out->max_ref = fr;
+        out->nonfinite = host[2];
+        const bool ok = host[2] == 0 && double(fe) <= cfg.tol * double(fr);
+        if (!ok) {
+            out->status = DS_EPARITY;
+            set_error("parity failed: max_err %.3g, max_ref %.3g, non-finite %u", double(fe),
+                      double(fr), host[2]);
+            return DS_OK;
+        }
+    }
+    if (cfg.slow_cut > 0 && best_so_far_ms > 0 && out->first_ms > cfg.slow_cut * best_so_far_ms) {
+        out->cut = 1;
+        out->number = 1;
+        out->repeats_ms[0] = out->first_ms;
+        summarise(out, 1);
+        return DS_OK;
+    }
+    // Warm-up, which also calibrates the number of launches per repeat.
+    double warm = out->first_ms;
+    if (cfg.warmup > 0) {
+        double w[1];
+        rc = time_repeats(launch, stream, cfg.warmup, 1, w);
+        if (rc != DS_OK) {
+            out->status = rc;
+            return DS_OK;
+        }
+        warm = w[0];
+    }
+    const double per = std::max(warm, 1e-4);
+    const int number = int(std::max(1.0, std::min(double(cfg.max_number),
+                                                  std::ceil(cfg.min_repeat_ms / per))));
+    rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
+    if (rc != DS_OK) {
+        out->status = rc;
+        return DS_OK;
+    }
+    out->number = number;
+    summarise(out, cfg.repeat);
+    return DS_OK;
+}
+
+int ds_empty_kernel_floor(hipStream_t stream, const ds_measure_cfg *cfg_in, ds_measurement *out) {
+    if (!out) {
+        set_error("null argument");
+        return DS_EINVAL;
+    }
+    std::memset(out, 0, sizeof *out);
+    ds_measure_cfg cfg;
+    if (cfg_in) cfg = *cfg_in;
+    else ds_measure_cfg_default(&cfg);
+    cfg.repeat = std::max(1, std::min(cfg.repeat, DS_MAX_REPEATS));
+    auto launch = [&]() {
+        hipLaunchKernelGGL(empty_kernel, dim3(1), dim3(64), 0, stream);
+        return hip_ok(hipGetLastError(), "empty launch") ? DS_OK : DS_EHIP;
+    };
+    double w[1];
+    int rc = time_repeats(launch, stream, std::max(1, cfg.warmup), 1, w);
+    if (rc != DS_OK) return rc;
+    const int number = std::max(1, std::min(cfg.max_number,
+                                            int(std::ceil(cfg.min_repeat_ms / std::max(w[0], 1e-4)))));
+    rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
+    if (rc != DS_OK) return rc;
+    out->number = number;
+    summarise(out, cfg.repeat);
+    return DS_OK;
+}
+
+int droplet_tune(int op, const int64_t *shape, const ds_sched *start, int budget, ds_sched *best,
+                 double *best_ms) {
+    if (!shape || !best || !best_ms || budget < 0) {
+        set_error("bad droplet_tune arguments");
+        return DS_EINVAL;
+    }
+    ds_space *space = nullptr;
+    int rc = sched_space_create(op, shape, op == DS_OP_CONV2D_NCHW ? 9 : 3, &space);
+    if (rc != DS_OK) return rc;
+    Space sp;
+    build_space(op, shape, op == DS_OP_CONV2D_NCHW ? 9 : 3, sp);
+    int64_t nx, nw, ny;
+    if (op == DS_OP_CONV2D_NCHW) {
+        const int64_t P = conv_out_dim(sp.shape[2], sp.shape[5], sp.shape[7], sp.shape[8]);
+        const int64_t Q = conv_out_dim(sp.shape[3], sp.shape[6], sp.shape[7], sp.shape[8]);
+        nx = sp.shape[0] * sp.shape[1] * sp.shape[2] * sp.shape[3];
+        nw = sp.shape[4] * sp.shape[1] * sp.shape[5] * sp.shape[6];
+        ny = sp.shape[0] * sp.shape[4] * P * Q;
+    } else {
+        nx = sp.shape[0] * sp.shape[2];
+        nw = sp.shape[2] * sp.shape[1];
+        ny = sp.shape[0] * sp.shape[1];
+    }
+    const uint64_t base = 240620037ull;
+    std::vector<float> hx(size_t(std::max<int64_t>(nx, 1))), hw(size_t(std::max<int64_t>(nw, 1)));
+    ds_gen_uniform(base, nx, hx.data());
+    ds_gen_uniform(op == DS_OP_CONV2D_NCHW ? base + 1 : base + 2, nw, hw.data());
+    void *dx = nullptr, *dw = nullptr, *dy = nullptr;
+    rc = DS_OK;
+    if (!hip_ok(hipMalloc(&dx, size_t(std::max<int64_t>(nx, 1)) * 4), "hipMalloc(x)") ||
+        !hip_ok(hipMalloc(&dw, size_t(std::max<int64_t>(nw, 1)) * 4), "hipMalloc(w)") ||
+        !hip_ok(hipMalloc(&dy, size_t(std::max<int64_t>(ny, 1)) * 4), "hipMalloc(y)"))
+        rc = DS_ENOMEM;
+    if (rc == DS_OK &&
+        (!hip_ok(hipMemcpy(dx, hx.data(), size_t(nx) * 4, hipMemcpyHostToDevice), "copy x") ||
+         !hip_ok(hipMemcpy(dw, hw.data(), size_t(nw) * 4, hipMemcpyHostToDevice), "copy w")))
+        rc = DS_EHIP;
+    if (rc == DS_OK) {
+        ds_tune_cfg cfg;
+        ds_tune_cfg_default(&cfg);
+        ds_tune_io io = {static_cast<float *>(dx), static_cast<float *>(dw),
+                         static_cast<float *>(dy), nullptr, nullptr};
+        ds_tune_result res;
+        rc = droplet_tune_ex(space, start, budget, &cfg, &io, nullptr, nullptr, &res, nullptr);
+        if (rc == DS_OK) {
+            *best = res.best;
+            *best_ms = res.best_ms;
+        }
+    }
+    free_device(dx);
+    free_device(dw);
+    free_device(dy);
+    sched_space_destroy(space);
+    return rc;
+}
+
+int ds_device_info(int *cus, int *clock_khz, char *arch, int arch_len) {
+    int dev;
+    int rc = current_device(dev);
+    if (rc != DS_OK) return rc;
+    hipDeviceProp_t prop;
+    if (!hip_ok(hipGetDeviceProperties(&prop, dev), "hipGetDeviceProperties")) return DS_EHIP;
+    if (cus) *cus = prop.multiProcessorCount;
+    if (clock_khz) *clock_khz = prop.clockRate;
+    if (arch && arch_len > 0) {
+        std::strncpy(arch, prop.gcnArchName, size_t(arch_len) - 1);
+        arch[arch_len - 1] = 0;
+    }
+    return DS_OK;
+}
+
+int ds_num_instances(void) { return count_instances(); }
+
+int sched_has_kernel(const ds_space *space, const ds_sched *s) {
+    const int v = sched_valid(space, s);
+    if (v <= 0) return v;
+    Plan plan;
+    const int rc = make_plan(s, nullptr, nullptr, nullptr, plan);
+    if (rc == DS_OK) return 1;
+    return rc == DS_EUNSUPPORTED ? 0 : rc;
+}
+
+void ds_shutdown(void) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return;
+    for (int d = 0; d < kMaxDevices; ++d) {
+        if (!g_parity_buf[d]) continue;
+        if (hipSetDevice(d) == hipSuccess) (void)hipFree(g_parity_buf[d]);
+        g_parity_buf[d] = nullptr;
+    }
+    (void)hipSetDevice(cur);
+    g_lds_attr.clear();
+}
+
+}  // extern "C"

@@ -1,0 +1,374 @@
+// NCHW fp32 conv2d kernel family for gfx950.
+//
+// y[n,k,p,q] = sum_{c,r,s} x[n,c,p*st-pd+r,q*st-pd+s] * w[k,c,r,s]
+//
+// One workgroup computes a tk x th x tw output tile (channels x rows x cols)
+// of one image, over the input-channel chunks of its reduction split.  The
+// reduction inside a chunk runs over kr = c_l*R*S + r*S + s; an offset table
+// in LDS turns kr into the position of the tap, so the loop has no division.
+//
+//   conv_valu: VALU FMA.  Lanes take pixels first, then groups of KPT output
+//              channels; each lane accumulates KPT x PPT outputs.
+//   conv_mfma: implicit GEMM on v_mfma_f32_16x16x4f32 (M = channels, N =
+//              pixels, K = kr).  Four waves split the pixels of the tile; a
+//              wave holds TKB x NPB 16x16 blocks.  Lane group g (lanes
+//              16g..16g+15) feeds reduction steps kr = 16*j + 4*g + v, v < 4,
+//              for both operands, so a 16-byte LDS read gives four steps of A.
+//
+// LDS layout (lds=1): [weights tk x wrow][input halo tc x hs x ws][zero][table red]
+//             (lds=0): [table red x {offset, info}]
+// A split (ks > 1) accumulates with atomics into a zero-filled y.
+#include <utility>
+
+#include "kern_common.h"
+
+namespace ds {
+
+namespace {
+
+__device__ __forceinline__ void conv_tile_coords(const ConvArgs &a, int &n, int &z, int &kt,
+                                                 int &pt, int &qt) {
+    int t = xcd_tile(blockIdx.x, gridDim.x);
+    kt = t % a.tiles_k;
+    t /= a.tiles_k;
+    qt = t % a.tiles_q;
+    t /= a.tiles_q;
+    pt = t % a.tiles_p;
+    t /= a.tiles_p;
+    z = t % a.ks;
+    n = t / a.ks;
+}
+
+// Offset table for one chunk (identical for every chunk).  real = tc*R*S taps;
+// entries real..red-1 are padding and read zero.
+__device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool lds) {
+    const int RS = a.R * a.S;
+    const int real = a.tc * RS;
+    for (int e = threadIdx.x; e < a.red; e += blockDim.x) {
+        const int c_l = e / RS, rs = e - c_l * RS;
+        const int r = rs / a.S, s = rs - r * a.S;
+        if (lds) {
+            tab[e] = e < real ? c_l * a.hs * a.ws + r * a.ws + s : a.tc * a.hs * a.ws;
+        } else {
+            tab[2 * e] = e < real ? c_l * a.H * a.W + r * a.W + s : 0;
+            tab[2 * e + 1] = e < real ? int(0x80000000u | unsigned(c_l << 16) | unsigned(r << 8) |
+                                            unsigned(s))
+                                      : 0;
+        }
+    }
+}
+
+// Stage the input halo of chunk c0 and the weights of the tile into LDS.
+__device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, int pt, int qt,
+                                            int c0, float *wt, float *xs) {
+    const int RS = a.R * a.S;
+    const int real = a.tc * RS;
+    const int hw = a.hs * a.ws;
+    const int nh = a.tc * hw;
+    const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
+    const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
+    for (int e = threadIdx.x; e < nh; e += blockDim.x) {
+        const int c_l = e / hw, rem = e - c_l * hw;
+        const int hy = rem / a.ws, hx = rem - hy * a.ws;
+        const int c = c0 + c_l, gy = hy0 + hy, gx = hx0 + hx;
+        float v = 0.f;
+        if (c < a.C && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W)
+            v = xn[((size_t)c * a.H + gy) * a.W + gx];
+        xs[e] = v;
+    }
+    if (threadIdx.x == 0) xs[nh] = 0.f;
+    const int nw = a.tk * a.red;
+    const int crs = a.C * RS;
+    for (int e = threadIdx.x; e < nw; e += blockDim.x) {
+        const int kl = e / a.red, kr = e - kl * a.red;
+        const int k = kt * a.tk + kl;
+        float v = 0.f;
+        if (k < a.K && kr < real && c0 * RS + kr < crs) v = a.w[(size_t)k * crs + c0 * RS + kr];
+        wt[kl * a.wrow + kr] = v;
+    }
+}
+
+template <int KPT, int PPT, int UF, int LDS>
+__global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
+    extern __shared__ float smem[];
+    int n, z, kt, pt, qt;
+    conv_tile_coords(a, n, z, kt, pt, qt);
+    const int ci0 = z * a.cps, ci1 = min(ci0 + a.cps, a.chunks);
+    if (ci0 >= ci1) return;
+
+    const int tid = threadIdx.x;
+    const int pl = tid % a.npl, g = tid / a.npl;
+    const int k0 = kt * a.tk + g * KPT;
+    const int PQ = a.P * a.Q;
+
+    int poff[PPT], iy0[PPT], ix0[PPT], oq[PPT];
+    bool pv[PPT];
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+        const int pix = pl + a.npl * j;
+        const int py = pix / a.tw, px = pix - py * a.tw;
+        const int p = pt * a.th + py, q = qt * a.tw + px;
+        pv[j] = pix < a.npx && p < a.P && q < a.Q;
+        poff[j] = py * a.st * a.ws + px * a.st;
+        iy0[j] = p * a.st - a.pd;
+        ix0[j] = q * a.st - a.pd;
+        oq[j] = p * a.Q + q;
+    }
+
+    float acc[KPT][PPT];
+#pragma unroll
+    for (int i = 0; i < KPT; ++i)
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) acc[i][j] = 0.f;
+
+    float *wt = smem;
+    float *xs = smem + a.tk * a.wrow;
+    int *tab = LDS ? reinterpret_cast<int *>(xs + a.tc * a.hs * a.ws + 1)
+                   : reinterpret_cast<int *>(smem);
+    build_table(a, tab, LDS);
+
+    const int RS = a.R * a.S;
+    const int crs = a.C * RS;
+    for (int ci = ci0; ci < ci1; ++ci) {
+        const int c0 = ci * a.tc;
+        if (LDS) {
+            __syncthreads();
+            stage_chunk(a, n, kt, pt, qt, c0, wt, xs);
+            __syncthreads();
+            const float *wg = wt + g * KPT * a.wrow;
+#pragma unroll UF
+            for (int kr = 0; kr < a.red; ++kr) {
+                const int off = tab[kr];
+                float xv[PPT];
+#pragma unroll
+                for (int j = 0; j < PPT; ++j) xv[j] = xs[off + poff[j]];
+#pragma unroll
+                for (int i = 0; i < KPT; ++i) {
+                    const float wv = wg[i * a.wrow + kr];
+#pragma unroll
+                    for (int j = 0; j < PPT; ++j) acc[i][j] = fmaf(wv, xv[j], acc[i][j]);
+                }
+            }
+        } else {
+            if (ci == ci0) __syncthreads();
+            const float *xc = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
+#pragma unroll UF
+            for (int kr = 0; kr < a.red; ++kr) {
+                const int goff = tab[2 * kr];
+                const unsigned info = unsigned(tab[2 * kr + 1]);
+                const int c_l = int((info >> 16) & 0x7fffu);
+                const int r = int((info >> 8) & 0xffu), s = int(info & 0xffu);
+                const bool cok = (info & 0x80000000u) && c0 + c_l < a.C;
+                float xv[PPT];
+#pragma unroll
+                for (int j = 0; j < PPT; ++j) {
+                    const int iy = iy0[j] + r, ix = ix0[j] + s;
+                    const bool ok = cok && pv[j] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
+                    xv[j] = ok ? xc[goff + iy0[j] * a.W + ix0[j]] : 0.f;
+                }
+#pragma unroll
+                for (int i = 0; i < KPT; ++i) {
+                    const int k = k0 + i;
+                    const float wv = (cok && k < a.K) ? a.w[(size_t)k * crs + c0 * RS + kr] : 0.f;
+#pragma unroll
+                    for (int j = 0; j < PPT; ++j) acc[i][j] = fmaf(wv, xv[j], acc[i][j]);
+                }
+            }
+        }
+    }
+
+    float *yn = a.y + (size_t)n * a.K * PQ;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+        const int k = k0 + i;
+        if (k >= a.K) continue;
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) {
+            if (!pv[j]) continue;
+            float *dst = yn + (size_t)k * PQ + oq[j];
+            if (a.atomic) atomicAdd(dst, acc[i][j]);
+            else *dst = acc[i][j];
+        }
+    }
+}
+
+template <int TKB, int NPB, int UF, int LDS>
+__global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
+    extern __shared__ float smem[];
+    int n, z, kt, pt, qt;
+    conv_tile_coords(a, n, z, kt, pt, qt);
+    const int ci0 = z * a.cps, ci1 = min(ci0 + a.cps, a.chunks);
+    if (ci0 >= ci1) return;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wid = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    const int PQ = a.P * a.Q;
+
+    int poff[NPB], iy0[NPB], ix0[NPB], oq[NPB];
+    bool pv[NPB];
+#pragma unroll
+    for (int b = 0; b < NPB; ++b) {
+        const int pix = (wid * NPB + b) * 16 + li;
+        const int py = pix / a.tw, px = pix - py * a.tw;
+        const int p = pt * a.th + py, q = qt * a.tw + px;
+        pv[b] = pix < a.npx && p < a.P && q < a.Q;
+        poff[b] = py * a.st * a.ws + px * a.st;
+        iy0[b] = p * a.st - a.pd;
+        ix0[b] = q * a.st - a.pd;
+        oq[b] = p * a.Q + q;
+    }
+
+    floatx4 acc[TKB][NPB];
+#pragma unroll
+    for (int i = 0; i < TKB; ++i)
+#pragma unroll
+        for (int b = 0; b < NPB; ++b) acc[i][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    float *wt = smem;
+    float *xs = smem + a.tk * a.wrow;
+    int *tab = LDS ? reinterpret_cast<int *>(xs + a.tc * a.hs * a.ws + 1)
+                   : reinterpret_cast<int *>(smem);
+    build_table(a, tab, LDS);
+
+    constexpr int UG = UF >= 4 ? UF / 4 : 1;   // 16-step groups unrolled
+    const int RS = a.R * a.S;
+    const int crs = a.C * RS;
+    const int ngroups = a.red / 16;
+    for (int ci = ci0; ci < ci1; ++ci) {
+        const int c0 = ci * a.tc;
+        if (LDS) {
+            __syncthreads();
+            stage_chunk(a, n, kt, pt, qt, c0, wt, xs);
+            __syncthreads();
+#pragma unroll UG
+            for (int kg = 0; kg < ngroups; ++kg) {
+                const int kb = kg * 16 + 4 * lg;
+                floatx4 av[TKB];
+#pragma unroll
+                for (int i = 0; i < TKB; ++i)
+                    av[i] = *reinterpret_cast<const floatx4 *>(wt + (i * 16 + li) * a.wrow + kb);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int off = tab[kb + v];
+                    float bv[NPB];
+#pragma unroll
+                    for (int b = 0; b < NPB; ++b) bv[b] = xs[off + poff[b]];
+#pragma unroll
+                    for (int i = 0; i < TKB; ++i)
+#pragma unroll
+                        for (int b = 0; b < NPB; ++b)
+                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][v], bv[b],
+                                                                            acc[i][b], 0, 0, 0);
+                }
+            }
+        } else {
+            if (ci == ci0) __syncthreads();
+            const float *xc = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
+#pragma unroll UG
+            for (int kg = 0; kg < ngroups; ++kg) {
+                const int kb = kg * 16 + 4 * lg;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int kr = kb + v;
+                    const int goff = tab[2 * kr];
+                    const unsigned info = unsigned(tab[2 * kr + 1]);
+                    const int c_l = int((info >> 16) & 0x7fffu);
+                    const int r = int((info >> 8) & 0xffu), s = int(info & 0xffu);
+                    const bool cok = (info & 0x80000000u) && c0 + c_l < a.C;
+                    float av[TKB];
+#pragma unroll
+                    for (int i = 0; i < TKB; ++i) {
+                        const int k = kt * a.tk + i * 16 + li;
+                        av[i] = (cok && k < a.K) ? a.w[(size_t)k * crs + c0 * RS + kr] : 0.f;
+                    }
+                    float bv[NPB];
+#pragma unroll
+                    for (int b = 0; b < NPB; ++b) {
+                        const int iy = iy0[b] + r, ix = ix0[b] + s;
+                        const bool ok = cok && pv[b] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
+                        bv[b] = ok ? xc[goff + iy0[b] * a.W + ix0[b]] : 0.f;
+                    }
+#pragma unroll
+                    for (int i = 0; i < TKB; ++i)
+#pragma unroll
+                        for (int b = 0; b < NPB; ++b)
+                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[b],
+                                                                            acc[i][b], 0, 0, 0);
+                }
+            }
+        }
+    }
+
+    // 16x16 block: lane holds rows 4*lg + v (channels), column li (pixel).
+    float *yn = a.y + (size_t)n * a.K * PQ;
+#pragma unroll
+    for (int i = 0; i < TKB; ++i)
+#pragma unroll
+        for (int b = 0; b < NPB; ++b) {
+            if (!pv[b]) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int k = kt * a.tk + i * 16 + 4 * lg + v;
+                if (k >= a.K) continue;
+                float *dst = yn + (size_t)k * PQ + oq[b];
+                if (a.atomic) atomicAdd(dst, acc[i][b][v]);
+                else *dst = acc[i][b][v];
+            }
+        }
+}
+
+// ---- instance registry --------------------------------------------------------
+// conv_valu slots: ((log2 KPT * 5 + log2 PPT) * 5 + log2 UF) * 2 + LDS
+// conv_mfma slots: ((log2 TKB * 7 + log2 NPB) * 5 + log2 UF) * 2 + LDS
+constexpr int kValuSlots = kConvValuSlots;
+constexpr int kMfmaSlots = kConvMfmaSlots;
+
+}  // namespace
+
+extern const void *g_conv_valu[kConvValuSlots];
+extern const void *g_conv_mfma[kConvMfmaSlots];
+
+#ifndef DS_SLICE
+#define DS_SLICE 0
+#define DS_NSLICES 1
+#endif
+
+namespace {
+
+template <int I>
+void reg_valu() {
+    constexpr int lds = I % 2, iuf = (I / 2) % 5, ippt = (I / 10) % 5, ikpt = I / 50;
+    constexpr int KPT = 1 << ikpt, PPT = 1 << ippt, UF = 1 << iuf;
+    if constexpr (KPT * PPT <= 64 && conv_uf_reachable(KPT * PPT, UF) && I % DS_NSLICES == DS_SLICE)
+        g_conv_valu[I] = reinterpret_cast<const void *>(&conv_valu<KPT, PPT, UF, lds>);
+}
+
+template <int I>
+void reg_mfma() {
+    constexpr int lds = I % 2, iuf = (I / 2) % 5, inpb = (I / 10) % 7, itkb = I / 70;
+    constexpr int TKB = 1 << itkb, NPB = 1 << inpb, UF = 1 << iuf;
+    if constexpr (TKB * NPB <= 32 && conv_uf_reachable(TKB * NPB, UF) && I % DS_NSLICES == DS_SLICE)
+        g_conv_mfma[I] = reinterpret_cast<const void *>(&conv_mfma<TKB, NPB, UF, lds>);
+}
+
+template <size_t... I>
+void reg_all(std::index_sequence<I...>) {
+    (reg_valu<int(I)>(), ...);
+}
+template <size_t... I>
+void reg_all_mfma(std::index_sequence<I...>) {
+    (reg_mfma<int(I)>(), ...);
+}
+
+struct Registrar {
+    Registrar() {
+        reg_all(std::make_index_sequence<kValuSlots>{});
+        reg_all_mfma(std::make_index_sequence<kMfmaSlots>{});
+    }
+};
+const Registrar registrar;
+
+}  // namespace
+
+}  // namespace ds

@@ -1,0 +1,375 @@
+// Row-major fp32 matmul kernel family for gfx950: C[M,N] = A[M,K] * B[K,N].
+//
+// A workgroup of 256 threads computes a BM x BN tile of C over the K-tiles of
+// its split.  Each K-tile (BK deep) is staged through LDS:
+//   As[BM][BK+4]  (k contiguous; the 4-float pad keeps 16-byte row reads of
+//                  eight consecutive rows on distinct banks),
+//   Bs[BK][BN]    (n contiguous).
+// With dbuf the next K-tile is loaded into registers while the current one is
+// consumed, then written to the other LDS stage (one barrier per K-tile).
+//
+//   mm_valu: VALU FMA; thread (ty, tx) of a 16x16 grid owns RM rows x RN
+//            columns (contiguous).
+//   mm_mfma: 2x2 waves, each a WM x WN tile of fp32 MFMA blocks
+//            (v_mfma_f32_32x32x2f32 when WM, WN >= 32, else
+//            v_mfma_f32_16x16x4f32).  Lane group g feeds k = kk + VEC*g + v
+//            (v < VEC) to both operands, so one VEC-wide LDS read of A serves
+//            VEC MFMA steps.
+// A split (ks > 1) accumulates with atomics into a zero-filled C.
+#include <utility>
+
+#include "kern_common.h"
+
+namespace ds {
+
+namespace {
+
+__device__ __forceinline__ void mm_tile_coords(const MatmulArgs &a, int &mt, int &nt, int &z) {
+    int t = xcd_tile(blockIdx.x, gridDim.x);
+    nt = t % a.tiles_n;
+    t /= a.tiles_n;
+    mt = t % a.tiles_m;
+    z = t / a.tiles_m;
+}
+
+// Global -> register staging of one K-tile (float4 slots; zero outside A, B).
+template <int BM, int BN, int BK>
+struct Stager {
+    static constexpr int A4 = BM * BK / 4, B4 = BK * BN / 4;
+    static constexpr int AL = (A4 + 255) / 256, BL = (B4 + 255) / 256;
+    floatx4 ra[AL], rb[BL];
+
+    __device__ __forceinline__ void load(const MatmulArgs &a, int m0, int n0, int kt) {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int u = 0; u < AL; ++u) {
+            const int e = tid + 256 * u;
+            floatx4 v = {0.f, 0.f, 0.f, 0.f};
+            if (A4 % 256 == 0 || e < A4) {
+                const int m = e / (BK / 4), k4 = e - m * (BK / 4);
+                const int gm = m0 + m, gk = kt * BK + 4 * k4;
+                if (gm < a.M) {
+                    const float *src = a.A + (size_t)gm * a.K + gk;
+                    if (a.vecA && gk + 3 < a.K) {
+                        v = *reinterpret_cast<const floatx4 *>(src);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (gk + i < a.K) v[i] = src[i];
+                    }
+                }
+            }
+            ra[u] = v;
+        }
+#pragma unroll
+        for (int u = 0; u < BL; ++u) {
+            const int e = tid + 256 * u;
+            floatx4 v = {0.f, 0.f, 0.f, 0.f};
+            if (B4 % 256 == 0 || e < B4) {
+                const int k = e / (BN / 4), n4 = e - k * (BN / 4);
+                const int gk = kt * BK + k, gn = n0 + 4 * n4;
+                if (gk < a.K) {
+                    const float *src = a.B + (size_t)gk * a.N + gn;
+                    if (a.vecB && gn + 3 < a.N) {
+                        v = *reinterpret_cast<const floatx4 *>(src);
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (gn + i < a.N) v[i] = src[i];
+                    }
+                }
+            }
+            rb[u] = v;
+        }
+    }
+
+    __device__ __forceinline__ void store(float *As, float *Bs) const {
+        const int tid = threadIdx.x;
+        constexpr int AS = BK + 4;
+#pragma unroll
+        for (int u = 0; u < AL; ++u) {
+            const int e = tid + 256 * u;
+            if (A4 % 256 == 0 || e < A4) {
+                const int m = e / (BK / 4), k4 = e - m * (BK / 4);
+                *reinterpret_cast<floatx4 *>(As + m * AS + 4 * k4) = ra[u];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < BL; ++u) {
+            const int e = tid + 256 * u;
+            if (B4 % 256 == 0 || e < B4) {
+                const int k = e / (BN / 4), n4 = e - k * (BN / 4);
+                *reinterpret_cast<floatx4 *>(Bs + k * BN + 4 * n4) = rb[u];
+            }
+        }
+    }
+};
+
+template <int RM, int RN, int BK, int UF, int DB>
+__global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
+    constexpr int BM = 16 * RM, BN = 16 * RN, AS = BK + 4;
+    constexpr int STAGE = BM * AS + BK * BN;
+    constexpr int U4 = UF >= 4 ? UF / 4 : 1;
+    extern __shared__ float smem[];
+    int mt, nt, z;
+    mm_tile_coords(a, mt, nt, z);
+    const int kt0 = z * a.kps, kt1 = min(kt0 + a.kps, a.nkt);
+    if (kt0 >= kt1) return;
+    const int m0 = mt * BM, n0 = nt * BN;
+    const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+
+    float acc[RM][RN];
+#pragma unroll
+    for (int i = 0; i < RM; ++i)
+#pragma unroll
+        for (int j = 0; j < RN; ++j) acc[i][j] = 0.f;
+
+    Stager<BM, BN, BK> st;
+    auto compute = [&](const float *As, const float *Bs) {
+#pragma unroll U4
+        for (int kk = 0; kk < BK; kk += 4) {
+            floatx4 av[RM];
+#pragma unroll
+            for (int i = 0; i < RM; ++i)
+                av[i] = *reinterpret_cast<const floatx4 *>(As + (ty * RM + i) * AS + kk);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float bv[RN];
+                const float *brow = Bs + (kk + v) * BN + tx * RN;
+                if constexpr (RN >= 4) {
+#pragma unroll
+                    for (int j = 0; j < RN; j += 4) {
+                        const floatx4 b4 = *reinterpret_cast<const floatx4 *>(brow + j);
+                        bv[j] = b4[0];
+                        bv[j + 1] = b4[1];
+                        bv[j + 2] = b4[2];
+                        bv[j + 3] = b4[3];
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < RN; ++j) bv[j] = brow[j];
+                }
+#pragma unroll
+                for (int i = 0; i < RM; ++i)
+#pragma unroll
+                    for (int j = 0; j < RN; ++j) acc[i][j] = fmaf(av[i][v], bv[j], acc[i][j]);
+            }
+        }
+    };
+
+    if (DB) {
+        st.load(a, m0, n0, kt0);
+        st.store(smem, smem + BM * AS);
+        __syncthreads();
+        for (int kt = kt0; kt < kt1; ++kt) {
+            const int s = (kt - kt0) & 1;
+            const bool more = kt + 1 < kt1;
+            if (more) st.load(a, m0, n0, kt + 1);
+            compute(smem + s * STAGE, smem + s * STAGE + BM * AS);
+            if (more) st.store(smem + (s ^ 1) * STAGE, smem + (s ^ 1) * STAGE + BM * AS);
+            __syncthreads();
+        }
+    } else {
+        for (int kt = kt0; kt < kt1; ++kt) {
+            st.load(a, m0, n0, kt);
+            __syncthreads();
+            st.store(smem, smem + BM * AS);
+            __syncthreads();
+            compute(smem, smem + BM * AS);
+        }
+    }
+
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+        const int gm = m0 + ty * RM + i;
+        if (gm >= a.M) continue;
+        float *crow = a.C + (size_t)gm * a.N;
+#pragma unroll
+        for (int j = 0; j < RN; ++j) {
+            const int gn = n0 + tx * RN + j;
+            if (gn >= a.N) continue;
+            if (a.atomic) atomicAdd(crow + gn, acc[i][j]);
+            else crow[gn] = acc[i][j];
+        }
+    }
+}
+
+template <int WM, int WN, int BK, int UF, int DB>
+__global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
+    constexpr int BM = 2 * WM, BN = 2 * WN, AS = BK + 4;
+    constexpr int STAGE = BM * AS + BK * BN;
+    constexpr bool BIG = WM >= 32 && WN >= 32;
+    constexpr int IM = BIG ? 32 : 16;          // MFMA output tile edge
+    constexpr int NG = 64 / IM;                // lane groups along k
+    constexpr int VEC = cmin(4, BK / NG);      // k values per lane per LDS read
+    constexpr int KG = NG * VEC;               // k consumed per group step
+    constexpr int MB = WM / IM, NB = WN / IM;
+    constexpr int KSTEP = BIG ? 2 : 4;
+    constexpr int UG = cmax(1, UF * KSTEP / KG);
+    using Acc = typename std::conditional<BIG, floatx16, floatx4>::type;
+
+    extern __shared__ float smem[];
+    int mt, nt, z;
+    mm_tile_coords(a, mt, nt, z);
+    const int kt0 = z * a.kps, kt1 = min(kt0 + a.kps, a.nkt);
+    if (kt0 >= kt1) return;
+    const int m0 = mt * BM, n0 = nt * BN;
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wr = wid >> 1, wc = wid & 1;
+    const int li = lane % IM, lg = lane / IM;
+
+    Acc acc[MB][NB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[i][j] = Acc{};
+
+    Stager<BM, BN, BK> st;
+    auto compute = [&](const float *As, const float *Bs) {
+#pragma unroll UG
+        for (int kk = 0; kk < BK; kk += KG) {
+            float av[MB][VEC];
+#pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                const float *src = As + (wr * WM + i * IM + li) * AS + kk + VEC * lg;
+                if constexpr (VEC == 4) {
+                    const floatx4 t = *reinterpret_cast<const floatx4 *>(src);
+                    av[i][0] = t[0];
+                    av[i][1] = t[1];
+                    av[i][2] = t[2];
+                    av[i][3] = t[3];
+                } else if constexpr (VEC == 2) {
+                    const float2 t = *reinterpret_cast<const float2 *>(src);
+                    av[i][0] = t.x;
+                    av[i][1] = t.y;
+                } else {
+                    av[i][0] = src[0];
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                float bv[NB];
+                const float *brow = Bs + (kk + VEC * lg + v) * BN + wc * WN + li;
+#pragma unroll
+                for (int j = 0; j < NB; ++j) bv[j] = brow[j * IM];
+#pragma unroll
+                for (int i = 0; i < MB; ++i)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        if constexpr (BIG)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][v], bv[j],
+                                                                            acc[i][j], 0, 0, 0);
+                        else
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][v], bv[j],
+                                                                            acc[i][j], 0, 0, 0);
+                    }
+            }
+        }
+    };
+
+    if (DB) {
+        st.load(a, m0, n0, kt0);
+        st.store(smem, smem + BM * AS);
+        __syncthreads();
+        for (int kt = kt0; kt < kt1; ++kt) {
+            const int s = (kt - kt0) & 1;
+            const bool more = kt + 1 < kt1;
+            if (more) st.load(a, m0, n0, kt + 1);
+            compute(smem + s * STAGE, smem + s * STAGE + BM * AS);
+            if (more) st.store(smem + (s ^ 1) * STAGE, smem + (s ^ 1) * STAGE + BM * AS);
+            __syncthreads();
+        }
+    } else {
+        for (int kt = kt0; kt < kt1; ++kt) {
+            st.load(a, m0, n0, kt);
+            __syncthreads();
+            st.store(smem, smem + BM * AS);
+            __syncthreads();
+            compute(smem, smem + BM * AS);
+        }
+    }
+
+    // Output layout: 32x32 block, lane holds rows 8*(v/4) + 4*lg + v%4 of
+    // column li (v < 16); 16x16 block, rows 4*lg + v of column li (v < 4).
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int gn = n0 + wc * WN + j * IM + li;
+            if (gn >= a.N) continue;
+            constexpr int NV = BIG ? 16 : 4;
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                const int row = BIG ? 8 * (v / 4) + 4 * lg + (v % 4) : 4 * lg + v;
+                const int gm = m0 + wr * WM + i * IM + row;
+                if (gm >= a.M) continue;
+                float *dst = a.C + (size_t)gm * a.N + gn;
+                if (a.atomic) atomicAdd(dst, acc[i][j][v]);
+                else *dst = acc[i][j][v];
+            }
+        }
+}
+
+}  // namespace
+
+extern const void *g_mm_valu[kMmValuSlots];
+extern const void *g_mm_mfma[kMmMfmaSlots];
+
+#ifndef DS_SLICE
+#define DS_SLICE 0
+#define DS_NSLICES 1
+#endif
+
+namespace {
+
+constexpr int kMmBkList[5] = {4, 8, 16, 32, 64};
+constexpr int kMmWaveList[4] = {16, 32, 64, 128};
+
+// slot = (((log2 RM * 5 + log2 RN) * 5 + ibk) * 7 + log2 UF) * 2 + DB
+template <int I>
+void reg_mm_valu() {
+    constexpr int DB = I % 2, iuf = (I / 2) % 7, ibk = (I / 14) % 5, irn = (I / 70) % 5,
+                  irm = I / 350;
+    constexpr int RM = 1 << irm, RN = 1 << irn, BK = kMmBkList[ibk], UF = 1 << iuf;
+    constexpr int lds = (DB ? 2 : 1) * (16 * RM * (BK + 4) + BK * 16 * RN) * 4;
+    if constexpr (RM * RN <= 128 && UF <= BK && lds <= kLdsLimit &&
+                  mm_uf_reachable(BK, RM * RN, UF) && I % DS_NSLICES == DS_SLICE)
+        g_mm_valu[I] = reinterpret_cast<const void *>(&mm_valu<RM, RN, BK, UF, DB>);
+}
+
+// slot = (((iwm * 4 + iwn) * 5 + ibk) * 7 + log2 UF) * 2 + DB
+template <int I>
+void reg_mm_mfma() {
+    constexpr int DB = I % 2, iuf = (I / 2) % 7, ibk = (I / 14) % 5, iwn = (I / 70) % 4,
+                  iwm = I / 280;
+    constexpr int WM = kMmWaveList[iwm], WN = kMmWaveList[iwn], BK = kMmBkList[ibk],
+                  UF = 1 << iuf;
+    constexpr bool BIG = WM >= 32 && WN >= 32;
+    constexpr int KSTEP = BIG ? 2 : 4;
+    constexpr int blocks = BIG ? (WM / 32) * (WN / 32) : (WM / 16) * (WN / 16);
+    constexpr int lds = (DB ? 2 : 1) * (2 * WM * (BK + 4) + BK * 2 * WN) * 4;
+    if constexpr (lds <= kLdsLimit && UF <= BK / KSTEP && mm_uf_reachable(BK / KSTEP, blocks, UF) &&
+                  I % DS_NSLICES == DS_SLICE)
+        g_mm_mfma[I] = reinterpret_cast<const void *>(&mm_mfma<WM, WN, BK, UF, DB>);
+}
+
+template <size_t... I>
+void reg_all_valu(std::index_sequence<I...>) {
+    (reg_mm_valu<int(I)>(), ...);
+}
+template <size_t... I>
+void reg_all_mfma(std::index_sequence<I...>) {
+    (reg_mm_mfma<int(I)>(), ...);
+}
+
+struct Registrar {
+    Registrar() {
+        reg_all_valu(std::make_index_sequence<kMmValuSlots>{});
+        reg_all_mfma(std::make_index_sequence<kMmMfmaSlots>{});
+    }
+};
+const Registrar registrar;
+
+}  // namespace
+
+}  // namespace ds
