@@ -14,6 +14,14 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+try:
+    # PyTorch ships its own HIP runtime (same soname).  Loading it before the
+    # library makes the library bind to that runtime, so device pointers and
+    # streams handed over from torch belong to the runtime the kernels use.
+    import torch as _torch  # noqa: F401
+except ImportError:  # plain C-ABI use without torch
+    _torch = None
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdroplet.so")
 

@@ -40,7 +40,9 @@ __device__ __forceinline__ void conv_tile_coords(const ConvArgs &a, int &n, int 
 }
 
 // Offset table for one chunk (identical for every chunk).  real = tc*R*S taps;
-// entries real..red-1 are padding and read zero.
+// entries real..red-1 are padding: their weights are zero, and in LDS mode they
+// point at the first halo element (a finite value inside the halo for every
+// pixel offset); in global mode their valid bit is clear and they read zero.
 __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool lds) {
     const int RS = a.R * a.S;
     const int real = a.tc * RS;
@@ -48,7 +50,7 @@ __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool ld
         const int c_l = e / RS, rs = e - c_l * RS;
         const int r = rs / a.S, s = rs - r * a.S;
         if (lds) {
-            tab[e] = e < real ? c_l * a.hs * a.ws + r * a.ws + s : a.tc * a.hs * a.ws;
+            tab[e] = e < real ? c_l * a.hs * a.ws + r * a.ws + s : 0;
         } else {
             tab[2 * e] = e < real ? c_l * a.H * a.W + r * a.W + s : 0;
             tab[2 * e + 1] = e < real ? int(0x80000000u | unsigned(c_l << 16) | unsigned(r << 8) |

@@ -240,3 +240,15 @@ def test_error_paths_without_gpu():
         lib.kernel_run(2, s.sched(s.origin()), 0, 0, 0, 0)    # op mismatch
     with pytest.raises(lib.DsError, match="DS_EINVAL"):
         lib.droplet_tune_ex(m, None, 10, None, None, None)   # GPU mode needs buffers
+
+
+def test_single_hip_runtime_in_process():
+    """Loading the binding first must not map a second HIP runtime next to torch's."""
+    import subprocess
+    import sys
+    code = ("import paper_2406_20037_amd as p; p._lib.ds_num_instances(); import torch, re; "
+            "print(len(set(re.findall(r'/\\S*libamdhip64\\S*', open('/proc/self/maps').read()))))")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=lib.HERE + "/..", timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1"

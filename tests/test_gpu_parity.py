@@ -1,0 +1,279 @@
+"""GPU parity of the HIP kernel family against the fp64 oracle, through the C ABI.
+
+Bar: max |y - ref| <= 1e-4 * max |ref| for U[-1,1) and He-normal inputs; exact
+equality for small-integer and all-ones inputs (every partial sum is an
+integer below 2**24, so every fp32 summation order is exact).  Outputs are
+NaN-prefilled (catches unwritten outputs) and followed by a canary tail
+(catches writes past the end).
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import synthdata
+from synthdata import workloads as wl
+from oracle import kernels as ok
+from oracle import space as osp
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+CANARY = 12345.0
+TAIL = 64
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    return torch
+
+
+@pytest.fixture(scope="module")
+def lib(torch_dev):
+    from paper_2406_20037_amd import _lib
+    return _lib
+
+
+def to_dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def out_elems(op, sh):
+    if op == 1:
+        P, Q = osp.conv_out(sh)
+        return sh[0] * sh[4] * P * Q
+    return sh[0] * sh[1]
+
+
+class Runner:
+    def __init__(self, torch, lib, op, sh, x, w):
+        self.torch, self.lib, self.op, self.sh = torch, lib, op, sh
+        self.space = lib.Space(op, sh)
+        self.x, self.w = to_dev(torch, x), to_dev(torch, w)
+        self.n = out_elems(op, sh)
+        self.ybuf = torch.empty(self.n + TAIL, dtype=torch.float32, device="cuda:0")
+
+    def run(self, idx):
+        t = self.torch
+        self.ybuf[: self.n].fill_(float("nan"))
+        self.ybuf[self.n:].fill_(CANARY)
+        self.lib.kernel_run(self.op, self.space.sched(idx), self.x, self.w, self.ybuf)
+        t.cuda.synchronize()
+        out = self.ybuf.cpu().numpy()
+        assert np.all(out[self.n:] == CANARY), "write past the end of y"
+        return out[: self.n].astype(np.float64)
+
+
+def pick_points(o, n_random, seed, per_value=2):
+    """Random valid points plus, for every axis value, a few valid points
+    taking it (so every knob value is exercised)."""
+    rng = np.random.default_rng(seed)
+    pts = set()
+    size = o.size()
+    tries = 0
+    while len(pts) < n_random and tries < 100 * n_random:
+        tries += 1
+        p = o.from_key(int(rng.integers(size)))
+        if o.valid(p):
+            pts.add(p)
+    for a, n in enumerate(o.sizes):
+        for v in range(n):
+            got, tries = 0, 0
+            while got < per_value and tries < 4000:
+                tries += 1
+                p = list(o.from_key(int(rng.integers(size))))
+                p[a] = v
+                p = tuple(p)
+                if o.valid(p):
+                    pts.add(p)
+                    got += 1
+    return sorted(pts)
+
+
+def check_close(y, ref, what):
+    scale = np.abs(ref).max()
+    err = np.abs(y - ref).max() if y.size else 0.0
+    assert np.all(np.isfinite(y)), f"{what}: non-finite output"
+    assert err <= TOL * scale, f"{what}: max err {err:.3g} vs max ref {scale:.3g}"
+
+
+PARITY_CASES = [
+    ("conv3x3_c64_56", 1, (1, 64, 56, 56, 64, 3, 3, 1, 1), 220),
+    ("conv7x7_s2_c3_224", 1, (1, 3, 224, 224, 64, 7, 7, 2, 3), 160),
+    ("matmul_1024", 2, (1024, 1024, 1024), 160),
+    ("conv_ragged", 1, (2, 5, 19, 23, 7, 3, 3, 2, 1), 250),
+    ("conv_ragged_5x5", 1, (1, 37, 15, 13, 40, 5, 5, 1, 2), 200),
+    ("conv_1x1_s2", 1, (1, 24, 17, 17, 48, 1, 1, 2, 0), 150),
+    ("matmul_ragged", 2, (129, 67, 300), 250),
+    ("matmul_fc", 2, (1, 1000, 2048), 120),
+    ("matmul_k_odd", 2, (33, 45, 7), 150),
+]
+
+
+@pytest.mark.parametrize("name,op,sh,n", PARITY_CASES, ids=[c[0] for c in PARITY_CASES])
+def test_parity_uniform(torch_dev, lib, name, op, sh, n):
+    if op == 1:
+        x, w = synthdata.conv_inputs(sh, "uniform")
+        ref = ok.conv2d_f64(x, w, sh).ravel()
+    else:
+        x, w = synthdata.matmul_inputs(sh, "uniform")
+        ref = ok.matmul_f64(x, w).ravel()
+    r = Runner(torch_dev, lib, op, sh, x, w)
+    o = osp.Space(op, sh)
+    pts = pick_points(o, n, seed=zlib.crc32(name.encode()) % 1000)
+    for p in pts:
+        print(name, o.knobs(p), flush=True)
+        check_close(r.run(p), ref, f"{name} {o.knobs(p)}")
+
+
+EXACT_CASES = [
+    ("conv3x3_c64_56", 1, (1, 64, 56, 56, 64, 3, 3, 1, 1)),
+    ("conv_ragged", 1, (2, 5, 19, 23, 7, 3, 3, 2, 1)),
+    ("conv7x7_s2", 1, (1, 3, 60, 60, 16, 7, 7, 2, 3)),
+    ("matmul_ragged", 2, (129, 67, 300)),
+    ("matmul_256", 2, (256, 256, 512)),
+]
+
+
+@pytest.mark.parametrize("kind", ["int", "ones"])
+@pytest.mark.parametrize("name,op,sh", EXACT_CASES, ids=[c[0] for c in EXACT_CASES])
+def test_parity_bit_exact(torch_dev, lib, name, op, sh, kind):
+    if op == 1:
+        x, w = synthdata.conv_inputs(sh, kind)
+        ref = ok.conv2d_f64(x, w, sh).ravel()
+    else:
+        x, w = synthdata.matmul_inputs(sh, kind)
+        ref = ok.matmul_f64(x, w).ravel()
+    assert np.abs(ref).max() < 2 ** 24
+    r = Runner(torch_dev, lib, op, sh, x, w)
+    o = osp.Space(op, sh)
+    for p in pick_points(o, 80, seed=3, per_value=1):
+        y = r.run(p)
+        assert np.array_equal(y, ref), f"{name} {kind} {o.knobs(p)}"
+
+
+def test_empty_batch_and_rows(torch_dev, lib):
+    torch = torch_dev
+    s = lib.Space(1, (0, 4, 8, 8, 4, 3, 3, 1, 1))
+    lib.kernel_run(1, s.sched(s.origin()), 0, 0, 0)
+    m = lib.Space(2, (0, 64, 64))
+    x = torch.zeros(1, device="cuda:0")
+    lib.kernel_run(2, m.sched(m.origin()), x, x, x)
+    torch.cuda.synchronize()
+
+
+def test_reference_kernels(torch_dev, lib):
+    torch = torch_dev
+    for op, sh in [(1, (2, 5, 19, 23, 7, 3, 3, 2, 1)), (2, (129, 67, 300))]:
+        if op == 1:
+            x, w = synthdata.conv_inputs(sh, "uniform")
+            ref = ok.conv2d_f64(x, w, sh).ravel()
+        else:
+            x, w = synthdata.matmul_inputs(sh, "uniform")
+            ref = ok.matmul_f64(x, w).ravel()
+        y = torch.empty(ref.size, device="cuda:0")
+        lib.kernel_run_reference(op, sh, to_dev(torch, x), to_dev(torch, w), y)
+        torch.cuda.synchronize()
+        check_close(y.cpu().numpy().astype(np.float64), ref, f"reference {sh}")
+
+
+MODEL_SCHEDULES = [
+    dict(tk=32, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1),
+    dict(tk=16, th=4, tw=16, tc=8, unroll=16, lds=1, ks=2, mfma=1),
+    dict(tk=8, th=4, tw=8, tc=8, unroll=16, lds=1, ks=1, mfma=0),
+    dict(tk=16, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1),
+]
+
+
+def nearest_valid(o, want):
+    """The valid point closest (breadth-first in index steps) to the point
+    whose knob values are nearest to want."""
+    target = tuple(v.index(want[n]) if want[n] in v else
+                   min(range(len(v)), key=lambda i: abs(np.log2(max(1, v[i])) -
+                                                        np.log2(max(1, want[n]))))
+                   for v, n in zip(o.values, o.names))
+    seen, frontier = {target}, [target]
+    while frontier:
+        for p in frontier:
+            if o.valid(p):
+                return p
+        nxt = []
+        for p in frontier:
+            for a in range(len(p)):
+                for d in (-1, 1):
+                    q = p[:a] + (p[a] + d,) + p[a + 1:]
+                    if 0 <= q[a] < o.sizes[a] and q not in seen:
+                        seen.add(q)
+                        nxt.append(q)
+        frontier = nxt
+    return None
+
+
+@pytest.mark.parametrize("name,op,sh,count", wl.RESNET50 + wl.VGG16,
+                         ids=[l[0] for l in wl.RESNET50] + ["vgg_" + l[0] for l in wl.VGG16])
+def test_model_layers_sampled(torch_dev, lib, name, op, sh, count):
+    """Full-size layers: sampled outputs against the oracle's one-by-one sums."""
+    if op == 1:
+        x, w = synthdata.conv_inputs(sh, "he")
+    else:
+        x, w = synthdata.matmul_inputs(sh, "he")
+    r = Runner(torch_dev, lib, op, sh, x, w)
+    o = osp.Space(op, sh)
+    rng = np.random.default_rng(11)
+    idx = np.unique(np.concatenate([rng.integers(0, r.n, 3000), [0, r.n - 1]])).astype(np.int64)
+    ref = ok.conv2d_f64_points(x, w, sh, idx) if op == 1 else ok.matmul_f64_points(x, w, idx)
+    scheds = MODEL_SCHEDULES if op == 1 else [
+        dict(bm=16, bn=64, bk=64, unroll=64, dbuf=1, mfma=0, ks=8),
+        dict(bm=16, bn=16, bk=16, unroll=16, dbuf=0, mfma=0, ks=1)]
+    seen = set()
+    for want in scheds:
+        p = nearest_valid(o, want)
+        if p in seen:
+            continue
+        seen.add(p)
+        print(name, o.knobs(p), flush=True)
+        y = r.run(p)
+        assert np.all(np.isfinite(y)), f"{name} {o.knobs(p)}: unwritten or non-finite output"
+        check_close(y[idx], ref, f"{name} {o.knobs(p)}")
+
+
+def test_measure_and_parity_detection(torch_dev, lib):
+    torch = torch_dev
+    op, sh = wl.SINGLE["conv3x3_c64_56"]
+    x, w = synthdata.conv_inputs(sh, "uniform")
+    ref = ok.conv2d_f64(x, w, sh).astype(np.float32).ravel()
+    s = lib.Space(op, sh)
+    xd, wd = to_dev(torch, x), to_dev(torch, w)
+    y = torch.empty(ref.size, device="cuda:0")
+    good = to_dev(torch, ref)
+    io = lib.make_io(xd, wd, y, good)
+    p = s.sched_of(tk=32, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1)
+    m = lib.ds_measure(p, io, lib.measure_cfg(repeat=7))
+    assert m.status == 0 and m.n_repeats == 7 and 0 < m.median_ms < 10
+    assert m.max_err <= 1e-4 * m.max_ref and m.nonfinite == 0
+    bad = to_dev(torch, ref + 1.0)
+    io_bad = lib.make_io(xd, wd, y, bad)
+    m = lib.ds_measure(p, io_bad, lib.measure_cfg(repeat=3))
+    assert m.status == lib.DS_EPARITY
+    floor = lib.ds_empty_kernel_floor()
+    assert 0 < floor.median_ms < 0.1
+
+
+def test_tune_small_budget(torch_dev, lib):
+    torch = torch_dev
+    op, sh = wl.SINGLE["conv3x3_c64_56"]
+    x, w = synthdata.conv_inputs(sh, "uniform")
+    s = lib.Space(op, sh)
+    y = torch.empty(out_elems(op, sh), device="cuda:0")
+    io = lib.make_io(to_dev(torch, x), to_dev(torch, w), y)
+    cfg = lib.tune_cfg(n_explore=24, budget=12, measure=lib.measure_cfg(repeat=5, min_repeat_ms=0.1))
+    res, trace = lib.ds_tune(s, cfg, io, trace_cap=128)
+    assert res.n_explore_measured == 24 and res.n_droplet_measured <= 12
+    assert res.best_ms <= res.seed_ms and res.n_failed == 0
+    assert all(t[1] == 0 for t in trace)
+    o = osp.Space(op, sh)
+    assert o.valid(res.best.index())
+    best, ms = lib.droplet_tune(2, (64, 64, 64), None, 6)
+    assert ms > 0 and osp.Space(2, (64, 64, 64)).valid(best.index())
