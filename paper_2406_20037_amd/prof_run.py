@@ -1,0 +1,60 @@
+"""Runs one schedule repeatedly (and a plain device copy of known size), for
+profiling a single kernel instance with rocprofv3.
+
+    python -m paper_2406_20037_amd.prof_run --workload matmul_1024 \
+        --sched bm=64,bn=32,bk=32,unroll=64,dbuf=1,mfma=1,ks=2 --iters 100
+
+The copy (torch's elementwise copy of --copy-mib MiB) gives the factor that
+relates the HBM counters to bytes actually moved.
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", default="matmul_1024")
+    ap.add_argument("--sched", required=True, help="knob=value,... (every axis)")
+    ap.add_argument("--iters", type=int, default=100)
+    ap.add_argument("--copy-mib", type=int, default=64)
+    args = ap.parse_args(argv)
+
+    import torch
+
+    import synthdata
+    from synthdata import workloads as wl
+    from paper_2406_20037_amd import _lib as L
+
+    op, shape = wl.SINGLE[args.workload]
+    knobs = {k: int(v) for k, v in (kv.split("=") for kv in args.sched.split(","))}
+    space = L.Space(op, shape)
+    s = space.sched_of(**knobs)
+    if op == wl.OP_CONV:
+        x, w = synthdata.conv_inputs(shape, "uniform")
+        N, C, H, W, K, R, S, st, pd = shape
+        n_out = N * K * ((H + 2 * pd - R) // st + 1) * ((W + 2 * pd - S) // st + 1)
+    else:
+        x, w = synthdata.matmul_inputs(shape, "uniform")
+        n_out = shape[0] * shape[1]
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    yd = torch.empty(n_out, device="cuda:0")
+    for _ in range(args.iters):
+        L.kernel_run(op, s, xd, wd, yd)
+    n = args.copy_mib * (1 << 20) // 4
+    a = torch.ones(n, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(args.iters):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(f"ran {args.iters} x {space.knobs(s)} and {args.iters} x copy of {args.copy_mib} MiB",
+          flush=True)
+
+
+if __name__ == "__main__":
+    sys.exit(main())

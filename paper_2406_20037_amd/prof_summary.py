@@ -1,0 +1,81 @@
+"""Summarises rocprofv3 SQLite outputs (kernel-trace stats and --pmc runs) as
+Markdown tables.
+
+    python -m paper_2406_20037_amd.prof_summary --trace RUN_results.db \
+        [--fetch FETCH_results.db --write WRITE_results.db --copy-mib 64] [--top 15]
+
+FETCH_SIZE / WRITE_SIZE are KiB per dispatch; each is scaled by the ratio of
+the known byte count of the plain copy kernel (``__amd_rocclr_copyBuffer`` of
+--copy-mib MiB) to what the same counter reads for it.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import sqlite3
+import sys
+
+COPY = "__amd_rocclr_copyBuffer"
+
+
+def short(name: str) -> str:
+    return (name.replace("ds::(anonymous namespace)::", "").replace("void ", "")
+            .replace("(ds::MatmulArgs)", "").replace("(ds::ConvArgs)", ""))
+
+
+def top_kernels(db, top):
+    """Rows of rocprofv3's top_kernels view (durations in microseconds)."""
+    cur = sqlite3.connect(db).cursor()
+    rows = list(cur.execute("select name, total_calls, total_duration, average, percentage "
+                            "from top_kernels"))
+    return rows[:top], len(rows)
+
+
+def counters(db):
+    cur = sqlite3.connect(db).cursor()
+    acc = collections.defaultdict(list)
+    for name, counter, value in cur.execute(
+            "select kernel_name, counter_name, value from counters_collection"):
+        acc[(name, counter)].append(float(value))
+    return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-mib", type=int, default=64)
+    ap.add_argument("--top", type=int, default=15)
+    args = ap.parse_args(argv)
+    rows, n = top_kernels(args.trace, args.top)
+    print(f"### Kernel trace ({n} distinct kernels; top {len(rows)} by total time)\n")
+    print("| kernel | calls | total us | avg us | % |")
+    print("|---|---:|---:|---:|---:|")
+    for name, calls, tot, avg, pct in rows:
+        print(f"| `{short(name)}` | {calls} | {tot:.1f} | {avg:.3f} | {pct:.1f} |")
+    if args.fetch and args.write:
+        copy_bytes_kib = args.copy_mib * 1024.0
+        f, fn = counters(args.fetch)
+        w, wn = counters(args.write)
+        fc = f.get((COPY, "FETCH_SIZE"))
+        wc = w.get((COPY, "WRITE_SIZE"))
+        ff = copy_bytes_kib / fc if fc else float("nan")
+        wf = copy_bytes_kib / wc if wc else float("nan")
+        print(f"\n### HBM counters (KiB per dispatch)\n")
+        print(f"Copy kernel of {args.copy_mib} MiB: FETCH_SIZE {fc:.1f} KiB -> read factor "
+              f"{ff:.3f}; WRITE_SIZE {wc:.1f} KiB -> write factor {wf:.3f}.\n")
+        print("| kernel | dispatches | FETCH_SIZE | WRITE_SIZE | read bytes (scaled) | "
+              "write bytes (scaled) |")
+        print("|---|---:|---:|---:|---:|---:|")
+        names = sorted({k[0] for k in f} | {k[0] for k in w})
+        for name in names:
+            fv = f.get((name, "FETCH_SIZE"), float("nan"))
+            wv = w.get((name, "WRITE_SIZE"), float("nan"))
+            print(f"| `{short(name)}` | {fn.get((name, 'FETCH_SIZE'), 0)} | {fv:.1f} | {wv:.1f} | "
+                  f"{fv * ff * 1024:.0f} | {wv * wf * 1024:.0f} |")
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
