@@ -181,6 +181,11 @@ typedef struct {
                               slow_cut * best_so_far is timed once only (4.0; 0 = never) */
     double tol;            /* parity: max|y-ref| <= tol * max|ref| (1e-4) */
     int32_t check;         /* 1: parity-check the first launch against ref */
+    int32_t graph;         /* 1: time each repeat as one replay of a HIP graph holding
+                              `number` launches, on a library-owned stream (after
+                              synchronising io->stream); the output of the last
+                              replay is parity-checked again.  0: launch from the host
+                              on io->stream (default 1) */
 } ds_measure_cfg;
 
 /* Fills cfg with the defaults above. */
@@ -222,7 +227,8 @@ typedef struct {
 int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cfg,
                double best_so_far_ms, ds_measurement *out);
 
-/* Per-launch time of an empty kernel in the same harness (the dispatch floor). */
+/* Per-launch time of an empty kernel in the same harness (the dispatch floor),
+ * host launches or graph replays as cfg->graph says. */
 int ds_empty_kernel_floor(hipStream_t stream, const ds_measure_cfg *cfg, ds_measurement *out);
 
 /* ---- tuning --------------------------------------------------------------- */

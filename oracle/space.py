@@ -285,7 +285,7 @@ def matmul_geometry(shape, v):
     else:
         uf = min(trip, _pow2floor(max(1, v["unroll"] // body)))
     stages = 2 if v["dbuf"] else 1
-    lds = stages * (bm * (bk + 4) + bk * bn) * 4
+    lds = stages * (bm * bk + bk * bn) * 4
     nkt = _cdiv(K, bk)
     grid = _cdiv(M, bm) * _cdiv(N, bn) * v["ks"]
     threads = 256

@@ -61,7 +61,7 @@ class ds_geometry(C.Structure):
 class ds_measure_cfg(C.Structure):
     _fields_ = [("warmup", C.c_int32), ("repeat", C.c_int32), ("min_repeat_ms", C.c_double),
                 ("max_number", C.c_int32), ("slow_cut", C.c_double), ("tol", C.c_double),
-                ("check", C.c_int32)]
+                ("check", C.c_int32), ("graph", C.c_int32)]
 
 
 class ds_measurement(C.Structure):
@@ -253,8 +253,11 @@ class Space:
 
     def __del__(self):
         h = getattr(self, "h", None)
-        if h:
-            lib.sched_space_destroy(h)
+        if h and lib is not None:
+            try:
+                lib.sched_space_destroy(h)
+            except Exception:   # interpreter shutdown
+                pass
             self.h = None
 
     def sched(self, idx):

@@ -82,6 +82,7 @@ struct MatmulArgs {
     int tiles_m, tiles_n, ks;
     int nkt, kps;         // K-tiles, K-tiles per split
     int vecA, vecB;       // 1: 16-byte loads along K of A / along N of B are legal
+    int direct;           // 1: every tile is full and aligned: K-tiles go straight to LDS
     int atomic;
 };
 

@@ -116,6 +116,7 @@ __global__ __launch_bounds__(256) void mm_ref_kernel(MatmulArgs a) {
 constexpr int kMaxDevices = 64;
 std::mutex g_mu;
 unsigned *g_parity_buf[kMaxDevices];     // 4 words per device, library-owned
+hipStream_t g_graph_stream[kMaxDevices];  // capture / replay stream per device
 std::set<std::pair<int, const void *>> g_lds_attr;
 
 int current_device(int &dev) {
@@ -138,6 +139,21 @@ int parity_buffer(unsigned **out) {
         g_parity_buf[dev] = static_cast<unsigned *>(p);
     }
     *out = g_parity_buf[dev];
+    return DS_OK;
+}
+
+int graph_stream(hipStream_t *out) {
+    int dev;
+    int rc = current_device(dev);
+    if (rc != DS_OK) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_graph_stream[dev]) {
+        hipStream_t st;
+        if (!hip_ok(hipStreamCreateWithFlags(&st, hipStreamNonBlocking), "hipStreamCreate"))
+            return DS_EHIP;
+        g_graph_stream[dev] = st;
+    }
+    *out = g_graph_stream[dev];
     return DS_OK;
 }
 
@@ -220,6 +236,43 @@ int time_repeats(F &&fn, hipStream_t stream, int number, int repeat, double *rep
     if (!hip_ok(hipEventSynchronize(E.ev[repeat]), "hipEventSynchronize")) return DS_EHIP;
     for (int r = 0; r < repeat; ++r) rep[r] = elapsed_ms(E.ev[r], E.ev[r + 1]) / number;
     return DS_OK;
+}
+
+// Times `repeat` replays of a graph holding `number` launches of fn(stream).
+template <class F>
+int time_graph(F &&fn, hipStream_t caller, int number, int repeat, double *rep) {
+    hipStream_t st;
+    int rc = graph_stream(&st);
+    if (rc != DS_OK) return rc;
+    if (!hip_ok(hipStreamSynchronize(caller), "hipStreamSynchronize")) return DS_EHIP;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    if (!hip_ok(hipStreamBeginCapture(st, hipStreamCaptureModeRelaxed), "hipStreamBeginCapture"))
+        return DS_EHIP;
+    for (int i = 0; i < number && rc == DS_OK; ++i) rc = fn(st);
+    const hipError_t ec = hipStreamEndCapture(st, &graph);
+    if (rc != DS_OK || !hip_ok(ec, "hipStreamEndCapture")) {
+        if (graph) (void)hipGraphDestroy(graph);
+        return rc != DS_OK ? rc : DS_EHIP;
+    }
+    rc = DS_OK;
+    if (!hip_ok(hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0), "hipGraphInstantiate"))
+        rc = DS_EHIP;
+    Events E;
+    if (rc == DS_OK && !E.make(repeat + 1)) rc = DS_EHIP;
+    if (rc == DS_OK && (!hip_ok(hipGraphLaunch(exec, st), "hipGraphLaunch") ||
+                        !hip_ok(hipEventRecord(E.ev[0], st), "hipEventRecord")))
+        rc = DS_EHIP;
+    for (int r = 0; r < repeat && rc == DS_OK; ++r)
+        if (!hip_ok(hipGraphLaunch(exec, st), "hipGraphLaunch") ||
+            !hip_ok(hipEventRecord(E.ev[r + 1], st), "hipEventRecord"))
+            rc = DS_EHIP;
+    if (rc == DS_OK && !hip_ok(hipStreamSynchronize(st), "hipStreamSynchronize")) rc = DS_EHIP;
+    if (rc == DS_OK)
+        for (int r = 0; r < repeat; ++r) rep[r] = elapsed_ms(E.ev[r], E.ev[r + 1]) / number;
+    if (exec) (void)hipGraphExecDestroy(exec);
+    (void)hipGraphDestroy(graph);
+    return rc;
 }
 
 void summarise(ds_measurement *out, int n) {
@@ -336,6 +389,7 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.kps = int(cdiv64(a.nkt, a.ks));
         a.vecA = (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
         a.vecB = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
+        a.direct = a.vecA && a.vecB && a.M % bm == 0 && a.N % bn == 0 && a.K % bk == 0;
         a.atomic = a.ks > 1;
         plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf)
                          : mm_valu_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf);
@@ -456,6 +510,42 @@ int kernel_run_reference(int op, const int64_t *shape, const float *x, const flo
     return hip_ok(hipGetLastError(), "reference launch") ? DS_OK : DS_EHIP;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Parity of y against ref (NaN/Inf count, max |y - ref|, max |ref|); synchronises.
+int parity_check(const float *y, const float *ref, int64_t n, double tol, hipStream_t stream,
+                 ds_measurement *out) {
+    unsigned *buf = nullptr;
+    int rc = parity_buffer(&buf);
+    if (rc != DS_OK) return rc;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, stream, buf, 4);
+    const int64_t blocks = std::min<int64_t>(cdiv64(n, 256), 1024);
+    hipLaunchKernelGGL(parity_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, y, ref, n, buf);
+    unsigned host[4] = {0, 0, 0, 0};
+    if (!hip_ok(hipGetLastError(), "parity launch") ||
+        !hip_ok(hipMemcpyAsync(host, buf, 16, hipMemcpyDeviceToHost, stream), "parity copy") ||
+        !hip_ok(hipStreamSynchronize(stream), "parity sync"))
+        return DS_EHIP;
+    float fe, fr;
+    std::memcpy(&fe, &host[0], 4);
+    std::memcpy(&fr, &host[1], 4);
+    out->max_err = std::max(out->max_err, double(fe));
+    out->max_ref = std::max(out->max_ref, double(fr));
+    out->nonfinite += host[2];
+    if (host[2] != 0 || !(double(fe) <= tol * double(fr))) {
+        set_error("parity failed: max_err %.3g, max_ref %.3g, non-finite %u", double(fe), double(fr),
+                  host[2]);
+        return DS_EPARITY;
+    }
+    return DS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cfg_in,
                double best_so_far_ms, ds_measurement *out) {
     if (!s || !io || !out) {
@@ -484,53 +574,25 @@ int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cf
     const hipStream_t stream = io->stream;
     const bool check = cfg.check && io->ref && plan.y_elems > 0;
     auto launch = [&]() { return launch_plan(plan, stream); };
+    auto launch_on = [&](hipStream_t st) { return launch_plan(plan, st); };
+    auto fail = [&](int code) {
+        out->status = code;
+        out->median_ms = out->mean_ms = out->min_ms = std::numeric_limits<double>::infinity();
+        return DS_OK;
+    };
 
     // Parity launch on a NaN-filled output.
     if (check) {
         rc = fill_async(io->y, plan.y_elems, std::numeric_limits<float>::quiet_NaN(), stream);
-        if (rc != DS_OK) {
-            out->status = rc;
-            return DS_OK;
-        }
+        if (rc != DS_OK) return fail(rc);
     }
     double first[1];
     rc = time_repeats(launch, stream, 1, 1, first);
-    if (rc != DS_OK) {
-        out->status = rc;
-        return DS_OK;
-    }
+    if (rc != DS_OK) return fail(rc);
     out->first_ms = first[0];
     if (check) {
-        unsigned *buf = nullptr;
-        rc = parity_buffer(&buf);
-        if (rc != DS_OK) {
-            out->status = rc;
-            return DS_OK;
-        }
-        hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, stream, buf, 4);
-        const int64_t blocks = std::min<int64_t>(cdiv64(plan.y_elems, 256), 1024);
-        hipLaunchKernelGGL(parity_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, io->y,
-                           io->ref, plan.y_elems, buf);
-        unsigned host[4] = {0, 0, 0, 0};
-        if (!hip_ok(hipGetLastError(), "parity launch") ||
-            !hip_ok(hipMemcpyAsync(host, buf, 16, hipMemcpyDeviceToHost, stream), "parity copy") ||
-            !hip_ok(hipStreamSynchronize(stream), "parity sync")) {
-            out->status = DS_EHIP;
-            return DS_OK;
-        }
-        float fe, fr;
-        std::memcpy(&fe, &host[0], 4);
-        std::memcpy(&fr, &host[1], 4);
-        out->max_err = fe;
-        out->max_ref = fr;
-        out->nonfinite = host[2];
-        const bool ok = host[2] == 0 && double(fe) <= cfg.tol * double(fr);
-        if (!ok) {
-            out->status = DS_EPARITY;
-            set_error("parity failed: max_err %.3g, max_ref %.3g, non-finite %u", double(fe),
-                      double(fr), host[2]);
-            return DS_OK;
-        }
+        rc = parity_check(io->y, io->ref, plan.y_elems, cfg.tol, stream, out);
+        if (rc != DS_OK) return fail(rc);
     }
     if (cfg.slow_cut > 0 && best_so_far_ms > 0 && out->first_ms > cfg.slow_cut * best_so_far_ms) {
         out->cut = 1;
@@ -544,19 +606,26 @@ int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cf
     if (cfg.warmup > 0) {
         double w[1];
         rc = time_repeats(launch, stream, cfg.warmup, 1, w);
-        if (rc != DS_OK) {
-            out->status = rc;
-            return DS_OK;
-        }
+        if (rc != DS_OK) return fail(rc);
         warm = w[0];
     }
     const double per = std::max(warm, 1e-4);
     const int number = int(std::max(1.0, std::min(double(cfg.max_number),
                                                   std::ceil(cfg.min_repeat_ms / per))));
-    rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
-    if (rc != DS_OK) {
-        out->status = rc;
-        return DS_OK;
+    if (cfg.graph) {
+        if (check) {
+            rc = fill_async(io->y, plan.y_elems, std::numeric_limits<float>::quiet_NaN(), stream);
+            if (rc != DS_OK) return fail(rc);
+        }
+        rc = time_graph(launch_on, stream, number, cfg.repeat, out->repeats_ms);
+        if (rc != DS_OK) return fail(rc);
+        if (check) {
+            rc = parity_check(io->y, io->ref, plan.y_elems, cfg.tol, stream, out);
+            if (rc != DS_OK) return fail(rc);
+        }
+    } else {
+        rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
+        if (rc != DS_OK) return fail(rc);
     }
     out->number = number;
     summarise(out, cfg.repeat);
@@ -573,16 +642,18 @@ int ds_empty_kernel_floor(hipStream_t stream, const ds_measure_cfg *cfg_in, ds_m
     if (cfg_in) cfg = *cfg_in;
     else ds_measure_cfg_default(&cfg);
     cfg.repeat = std::max(1, std::min(cfg.repeat, DS_MAX_REPEATS));
-    auto launch = [&]() {
-        hipLaunchKernelGGL(empty_kernel, dim3(1), dim3(64), 0, stream);
+    auto launch_on = [&](hipStream_t st) {
+        hipLaunchKernelGGL(empty_kernel, dim3(1), dim3(64), 0, st);
         return hip_ok(hipGetLastError(), "empty launch") ? DS_OK : DS_EHIP;
     };
+    auto launch = [&]() { return launch_on(stream); };
     double w[1];
     int rc = time_repeats(launch, stream, std::max(1, cfg.warmup), 1, w);
     if (rc != DS_OK) return rc;
     const int number = std::max(1, std::min(cfg.max_number,
                                             int(std::ceil(cfg.min_repeat_ms / std::max(w[0], 1e-4)))));
-    rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
+    if (cfg.graph) rc = time_graph(launch_on, stream, number, cfg.repeat, out->repeats_ms);
+    else rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
     if (rc != DS_OK) return rc;
     out->number = number;
     summarise(out, cfg.repeat);
@@ -676,9 +747,13 @@ void ds_shutdown(void) {
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return;
     for (int d = 0; d < kMaxDevices; ++d) {
-        if (!g_parity_buf[d]) continue;
-        if (hipSetDevice(d) == hipSuccess) (void)hipFree(g_parity_buf[d]);
+        if (!g_parity_buf[d] && !g_graph_stream[d]) continue;
+        if (hipSetDevice(d) == hipSuccess) {
+            if (g_parity_buf[d]) (void)hipFree(g_parity_buf[d]);
+            if (g_graph_stream[d]) (void)hipStreamDestroy(g_graph_stream[d]);
+        }
         g_parity_buf[d] = nullptr;
+        g_graph_stream[d] = nullptr;
     }
     (void)hipSetDevice(cur);
     g_lds_attr.clear();

@@ -2,11 +2,16 @@
 //
 // A workgroup of 256 threads computes a BM x BN tile of C over the K-tiles of
 // its split.  Each K-tile (BK deep) is staged through LDS:
-//   As[BM][BK+4]  (k contiguous; the 4-float pad keeps 16-byte row reads of
-//                  eight consecutive rows on distinct banks),
-//   Bs[BK][BN]    (n contiguous).
-// With dbuf the next K-tile is loaded into registers while the current one is
-// consumed, then written to the other LDS stage (one barrier per K-tile).
+//   As[BM][BK]  k contiguous in 16-byte slots; slot j of row r is stored at
+//               j ^ swz(r), so the 16-byte reads of eight consecutive rows at
+//               one k land on distinct banks without padding,
+//   Bs[BK][BN]  n contiguous.
+// When every tile is full and the operands are 16-byte aligned (a.direct), the
+// K-tiles travel straight from global memory into LDS (global_load_lds, no
+// register staging); with dbuf the next K-tile is in flight while the current
+// one is consumed.  Otherwise tiles are staged through registers with bounds
+// checks (zero outside A and B) and, with dbuf, written to the other LDS stage
+// after the current one is consumed.
 //
 //   mm_valu: VALU FMA; thread (ty, tx) of a 16x16 grid owns RM rows x RN
 //            columns (contiguous).
@@ -24,12 +29,69 @@ namespace ds {
 
 namespace {
 
+#define DS_GLOBAL(p) ((const __attribute__((address_space(1))) void *)(p))
+#define DS_LOCAL(p) ((__attribute__((address_space(3))) void *)(p))
+
 __device__ __forceinline__ void mm_tile_coords(const MatmulArgs &a, int &mt, int &nt, int &z) {
     int t = xcd_tile(blockIdx.x, gridDim.x);
     nt = t % a.tiles_n;
     t /= a.tiles_n;
     mt = t % a.tiles_m;
     z = t / a.tiles_m;
+}
+
+// Slot permutation of A row r (BK/4 slots per row).
+template <int BK>
+__device__ __forceinline__ int a_swz(int r) {
+    constexpr int SPR = BK / 4;
+    if constexpr (SPR >= 8) return r & 7;
+    else return ((r * SPR) >> 3) & (SPR - 1);
+}
+
+// Float offset of A element (row, k) inside a stage.
+template <int BK>
+__device__ __forceinline__ int a_off(int row, int k) {
+    return row * BK + (((k >> 2) ^ a_swz<BK>(row)) << 2) + (k & 3);
+}
+
+// Waits for every vector-memory operation of the wave, then for LDS, then
+// barriers the workgroup without a memory fence (the waits above make the LDS
+// writes of every wave complete before any wave passes).
+__device__ __forceinline__ void stage_barrier() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Global -> LDS copy of one full, aligned K-tile (16 bytes per lane per
+// instruction; the LDS destination of a wave's instruction is contiguous).
+template <int BM, int BN, int BK>
+__device__ __forceinline__ void direct_load(const MatmulArgs &a, int m0, int n0, int kt, float *As,
+                                            float *Bs) {
+    constexpr int SPR = BK / 4, A4 = BM * SPR, B4 = BK * BN / 4;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+    for (int j = 0; j < (A4 + 255) / 256; ++j) {
+        const int base = j * 256 + wid * 64;
+        const int c = base + lane;
+        if (A4 % 256 == 0 || c < A4) {
+            const int row = c / SPR, slot = c % SPR;
+            const float *src = a.A + (size_t)(m0 + row) * a.K + kt * BK + 4 * (slot ^ a_swz<BK>(row));
+            __builtin_amdgcn_global_load_lds(DS_GLOBAL(src), DS_LOCAL(As + base * 4), 16, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < (B4 + 255) / 256; ++j) {
+        const int base = j * 256 + wid * 64;
+        const int c = base + lane;
+        if (B4 % 256 == 0 || c < B4) {
+            const int k = c / (BN / 4), n4 = c % (BN / 4);
+            const float *src = a.B + (size_t)(kt * BK + k) * a.N + n0 + 4 * n4;
+            __builtin_amdgcn_global_load_lds(DS_GLOBAL(src), DS_LOCAL(Bs + base * 4), 16, 0, 0);
+        }
+    }
 }
 
 // Global -> register staging of one K-tile (float4 slots; zero outside A, B).
@@ -85,13 +147,12 @@ struct Stager {
 
     __device__ __forceinline__ void store(float *As, float *Bs) const {
         const int tid = threadIdx.x;
-        constexpr int AS = BK + 4;
 #pragma unroll
         for (int u = 0; u < AL; ++u) {
             const int e = tid + 256 * u;
             if (A4 % 256 == 0 || e < A4) {
                 const int m = e / (BK / 4), k4 = e - m * (BK / 4);
-                *reinterpret_cast<floatx4 *>(As + m * AS + 4 * k4) = ra[u];
+                *reinterpret_cast<floatx4 *>(As + a_off<BK>(m, 4 * k4)) = ra[u];
             }
         }
 #pragma unroll
@@ -105,10 +166,61 @@ struct Stager {
     }
 };
 
+// The K-loop shared by both families: stages K-tiles [kt0, kt1) through LDS
+// and calls compute(As, Bs) on each.
+template <int BM, int BN, int BK, int DB, class F>
+__device__ __forceinline__ void k_loop(const MatmulArgs &a, int m0, int n0, int kt0, int kt1,
+                                       float *smem, F &&compute) {
+    constexpr int STAGE = BM * BK + BK * BN;
+    if (a.direct) {
+        if (DB) {
+            direct_load<BM, BN, BK>(a, m0, n0, kt0, smem, smem + BM * BK);
+            for (int kt = kt0; kt < kt1; ++kt) {
+                const int s = (kt - kt0) & 1;
+                stage_barrier();
+                if (kt + 1 < kt1) {
+                    float *nx = smem + (s ^ 1) * STAGE;
+                    direct_load<BM, BN, BK>(a, m0, n0, kt + 1, nx, nx + BM * BK);
+                }
+                compute(smem + s * STAGE, smem + s * STAGE + BM * BK);
+            }
+        } else {
+            for (int kt = kt0; kt < kt1; ++kt) {
+                stage_barrier();
+                direct_load<BM, BN, BK>(a, m0, n0, kt, smem, smem + BM * BK);
+                stage_barrier();
+                compute(smem, smem + BM * BK);
+            }
+        }
+        return;
+    }
+    Stager<BM, BN, BK> st;
+    if (DB) {
+        st.load(a, m0, n0, kt0);
+        st.store(smem, smem + BM * BK);
+        __syncthreads();
+        for (int kt = kt0; kt < kt1; ++kt) {
+            const int s = (kt - kt0) & 1;
+            const bool more = kt + 1 < kt1;
+            if (more) st.load(a, m0, n0, kt + 1);
+            compute(smem + s * STAGE, smem + s * STAGE + BM * BK);
+            if (more) st.store(smem + (s ^ 1) * STAGE, smem + (s ^ 1) * STAGE + BM * BK);
+            __syncthreads();
+        }
+    } else {
+        for (int kt = kt0; kt < kt1; ++kt) {
+            st.load(a, m0, n0, kt);
+            __syncthreads();
+            st.store(smem, smem + BM * BK);
+            __syncthreads();
+            compute(smem, smem + BM * BK);
+        }
+    }
+}
+
 template <int RM, int RN, int BK, int UF, int DB>
 __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
-    constexpr int BM = 16 * RM, BN = 16 * RN, AS = BK + 4;
-    constexpr int STAGE = BM * AS + BK * BN;
+    constexpr int BM = 16 * RM, BN = 16 * RN;
     constexpr int U4 = UF >= 4 ? UF / 4 : 1;
     extern __shared__ float smem[];
     int mt, nt, z;
@@ -124,14 +236,13 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
 #pragma unroll
         for (int j = 0; j < RN; ++j) acc[i][j] = 0.f;
 
-    Stager<BM, BN, BK> st;
     auto compute = [&](const float *As, const float *Bs) {
 #pragma unroll U4
         for (int kk = 0; kk < BK; kk += 4) {
             floatx4 av[RM];
 #pragma unroll
             for (int i = 0; i < RM; ++i)
-                av[i] = *reinterpret_cast<const floatx4 *>(As + (ty * RM + i) * AS + kk);
+                av[i] = *reinterpret_cast<const floatx4 *>(As + a_off<BK>(ty * RM + i, kk));
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 float bv[RN];
@@ -156,28 +267,7 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
             }
         }
     };
-
-    if (DB) {
-        st.load(a, m0, n0, kt0);
-        st.store(smem, smem + BM * AS);
-        __syncthreads();
-        for (int kt = kt0; kt < kt1; ++kt) {
-            const int s = (kt - kt0) & 1;
-            const bool more = kt + 1 < kt1;
-            if (more) st.load(a, m0, n0, kt + 1);
-            compute(smem + s * STAGE, smem + s * STAGE + BM * AS);
-            if (more) st.store(smem + (s ^ 1) * STAGE, smem + (s ^ 1) * STAGE + BM * AS);
-            __syncthreads();
-        }
-    } else {
-        for (int kt = kt0; kt < kt1; ++kt) {
-            st.load(a, m0, n0, kt);
-            __syncthreads();
-            st.store(smem, smem + BM * AS);
-            __syncthreads();
-            compute(smem, smem + BM * AS);
-        }
-    }
+    k_loop<BM, BN, BK, DB>(a, m0, n0, kt0, kt1, smem, compute);
 
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
@@ -196,8 +286,7 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
 
 template <int WM, int WN, int BK, int UF, int DB>
 __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
-    constexpr int BM = 2 * WM, BN = 2 * WN, AS = BK + 4;
-    constexpr int STAGE = BM * AS + BK * BN;
+    constexpr int BM = 2 * WM, BN = 2 * WN;
     constexpr bool BIG = WM >= 32 && WN >= 32;
     constexpr int IM = BIG ? 32 : 16;          // MFMA output tile edge
     constexpr int NG = 64 / IM;                // lane groups along k
@@ -224,14 +313,13 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
 #pragma unroll
         for (int j = 0; j < NB; ++j) acc[i][j] = Acc{};
 
-    Stager<BM, BN, BK> st;
     auto compute = [&](const float *As, const float *Bs) {
 #pragma unroll UG
         for (int kk = 0; kk < BK; kk += KG) {
             float av[MB][VEC];
 #pragma unroll
             for (int i = 0; i < MB; ++i) {
-                const float *src = As + (wr * WM + i * IM + li) * AS + kk + VEC * lg;
+                const float *src = As + a_off<BK>(wr * WM + i * IM + li, kk + VEC * lg);
                 if constexpr (VEC == 4) {
                     const floatx4 t = *reinterpret_cast<const floatx4 *>(src);
                     av[i][0] = t[0];
@@ -266,28 +354,7 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
             }
         }
     };
-
-    if (DB) {
-        st.load(a, m0, n0, kt0);
-        st.store(smem, smem + BM * AS);
-        __syncthreads();
-        for (int kt = kt0; kt < kt1; ++kt) {
-            const int s = (kt - kt0) & 1;
-            const bool more = kt + 1 < kt1;
-            if (more) st.load(a, m0, n0, kt + 1);
-            compute(smem + s * STAGE, smem + s * STAGE + BM * AS);
-            if (more) st.store(smem + (s ^ 1) * STAGE, smem + (s ^ 1) * STAGE + BM * AS);
-            __syncthreads();
-        }
-    } else {
-        for (int kt = kt0; kt < kt1; ++kt) {
-            st.load(a, m0, n0, kt);
-            __syncthreads();
-            st.store(smem, smem + BM * AS);
-            __syncthreads();
-            compute(smem, smem + BM * AS);
-        }
-    }
+    k_loop<BM, BN, BK, DB>(a, m0, n0, kt0, kt1, smem, compute);
 
     // Output layout: 32x32 block, lane holds rows 8*(v/4) + 4*lg + v%4 of
     // column li (v < 16); 16x16 block, rows 4*lg + v of column li (v < 4).
@@ -331,7 +398,7 @@ void reg_mm_valu() {
     constexpr int DB = I % 2, iuf = (I / 2) % 7, ibk = (I / 14) % 5, irn = (I / 70) % 5,
                   irm = I / 350;
     constexpr int RM = 1 << irm, RN = 1 << irn, BK = kMmBkList[ibk], UF = 1 << iuf;
-    constexpr int lds = (DB ? 2 : 1) * (16 * RM * (BK + 4) + BK * 16 * RN) * 4;
+    constexpr int lds = (DB ? 2 : 1) * (16 * RM * BK + BK * 16 * RN) * 4;
     if constexpr (RM * RN <= 128 && UF <= BK && lds <= kLdsLimit &&
                   mm_uf_reachable(BK, RM * RN, UF) && I % DS_NSLICES == DS_SLICE)
         g_mm_valu[I] = reinterpret_cast<const void *>(&mm_valu<RM, RN, BK, UF, DB>);
@@ -347,7 +414,7 @@ void reg_mm_mfma() {
     constexpr bool BIG = WM >= 32 && WN >= 32;
     constexpr int KSTEP = BIG ? 2 : 4;
     constexpr int blocks = BIG ? (WM / 32) * (WN / 32) : (WM / 16) * (WN / 16);
-    constexpr int lds = (DB ? 2 : 1) * (2 * WM * (BK + 4) + BK * 2 * WN) * 4;
+    constexpr int lds = (DB ? 2 : 1) * (2 * WM * BK + BK * 2 * WN) * 4;
     if constexpr (lds <= kLdsLimit && UF <= BK / KSTEP && mm_uf_reachable(BK / KSTEP, blocks, UF) &&
                   I % DS_NSLICES == DS_SLICE)
         g_mm_mfma[I] = reinterpret_cast<const void *>(&mm_mfma<WM, WN, BK, UF, DB>);

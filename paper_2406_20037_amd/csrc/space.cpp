@@ -162,7 +162,7 @@ Geometry mm_geometry(const int64_t *sh, const int32_t *v) {
     else
         g.unroll_eff = std::min(trip, pow2_floor(std::max(1, unroll / body)));
     const int stages = dbuf ? 2 : 1;
-    g.lds_bytes = stages * (bm * (bk + 4) + bk * bn) * 4;
+    g.lds_bytes = stages * (bm * bk + bk * bn) * 4;
     g.red = kstep;
     g.chunks = cdiv(K, bk);
     g.grid = cdiv(M, bm) * cdiv(N, bn) * ks;

@@ -271,6 +271,7 @@ void ds_measure_cfg_default(ds_measure_cfg *cfg) {
     cfg->slow_cut = 4.0;
     cfg->tol = 1e-4;
     cfg->check = 1;
+    cfg->graph = 1;
 }
 
 void ds_tune_cfg_default(ds_tune_cfg *cfg) {

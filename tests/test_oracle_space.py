@@ -109,14 +109,14 @@ def test_conv_geometry_hand_computed():
 def test_matmul_geometry_hand_computed():
     m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
     g = m.geometry(idx_of(m, bm=64, bn=64, bk=16, unroll=64, dbuf=1, mfma=1, ks=1))
-    assert g == dict(valid=True, grid=256, threads=256, lds_bytes=2 * (64 * 20 + 16 * 64) * 4,
+    assert g == dict(valid=True, grid=256, threads=256, lds_bytes=2 * (64 * 16 + 16 * 64) * 4,
                      acc=16, unroll_eff=8, t0=32, t1=32, red=2, chunks=64)
     g = m.geometry(idx_of(m, bm=32, bn=128, bk=32, unroll=16, dbuf=0, mfma=1, ks=4))
     # wave tile 16x64 -> 16x16x4 blocks: 1*4, acc 16; trip 8, 8*4 > 16 -> 16//4 = 4.
-    assert g == dict(valid=True, grid=32 * 8 * 4, threads=256, lds_bytes=(32 * 36 + 32 * 128) * 4,
+    assert g == dict(valid=True, grid=32 * 8 * 4, threads=256, lds_bytes=(32 * 32 + 32 * 128) * 4,
                      acc=16, unroll_eff=4, t0=16, t1=64, red=4, chunks=32)
     g = m.geometry(idx_of(m, bm=128, bn=64, bk=8, unroll=512, dbuf=0, mfma=0, ks=1))
-    assert g == dict(valid=True, grid=8 * 16, threads=256, lds_bytes=(128 * 12 + 8 * 64) * 4,
+    assert g == dict(valid=True, grid=8 * 16, threads=256, lds_bytes=(128 * 8 + 8 * 64) * 4,
                      acc=32, unroll_eff=8, t0=8, t1=4, red=1, chunks=128)
     assert not m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=0, ks=1))  # acc 256
     assert m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=1, ks=1))      # AGPRs
