@@ -59,6 +59,22 @@ ds_sched make_sched(const Space &sp, const int32_t *idx);
 bool sched_matches(const Space &sp, const ds_sched *s);
 
 // ---- launch plans -------------------------------------------------------------
+// Division by a run-time invariant d in [1, 2^31) for dividends n in [0, 2^31)
+// (Granlund & Montgomery, "Division by invariant integers using
+// multiplication", PLDI 1994): q = (umulhi(n, m) + n) >> s with
+// s = ceil(log2 d), m = floor(2^32 (2^s - d) / d) + 1.
+struct FastDiv {
+    uint32_t m;
+    int s;
+};
+
+inline FastDiv make_fastdiv(int d) {
+    int s = 0;
+    while ((int64_t(1) << s) < d) ++s;
+    const uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << s) - uint64_t(d))) / uint64_t(d) + 1;
+    return FastDiv{uint32_t(m), s};
+}
+
 // Arguments of the conv kernels (passed by value).
 struct ConvArgs {
     const float *x;
@@ -71,7 +87,9 @@ struct ConvArgs {
     int red, wrow;        // reduction length per chunk, LDS weight row stride
     int hs, ws;           // halo tile extent
     int npx, npl;         // pixels per tile, lanes covering pixels (VALU)
+    int ltw;              // log2(tw)
     int atomic;           // 1: accumulate into a zero-filled y
+    FastDiv f_hw, f_ws, f_red, f_rs, f_s;   // divisions by hs*ws, ws, red, R*S, S
 };
 
 struct MatmulArgs {

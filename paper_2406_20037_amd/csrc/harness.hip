@@ -37,9 +37,19 @@ bool hip_ok(hipError_t e, const char *what) {
 
 // ---- small kernels ------------------------------------------------------------
 
+// Fills n floats with v: 16-byte stores over the aligned body, scalar head and tail.
 __global__ void fill_kernel(float *p, int64_t n, float v) {
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+    const int64_t tid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t head = int64_t((16 - (reinterpret_cast<uintptr_t>(p) & 15)) & 15) / 4;
+    const int64_t h = head < n ? head : n;
+    const int64_t body = (n - h) / 4;
+    floatx4 *q = reinterpret_cast<floatx4 *>(p + h);
+    const floatx4 v4 = {v, v, v, v};
+    for (int64_t i = tid; i < body; i += stride) q[i] = v4;
+    if (tid < h) p[tid] = v;
+    const int64_t t0 = h + 4 * body;
+    if (tid < n - t0) p[t0 + tid] = v;
 }
 
 __global__ void fill_u32_kernel(unsigned *p, int n) {
@@ -372,6 +382,12 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.ws = (a.tw - 1) * a.st + a.S;
         a.npx = a.th * a.tw;
         a.npl = std::min(a.npx, 256);
+        a.ltw = log2_exact(a.tw);
+        a.f_hw = make_fastdiv(a.hs * a.ws);
+        a.f_ws = make_fastdiv(a.ws);
+        a.f_red = make_fastdiv(a.red);
+        a.f_rs = make_fastdiv(a.R * a.S);
+        a.f_s = make_fastdiv(a.S);
         a.atomic = a.ks > 1;
         plan.func = mfma ? conv_mfma_instance(g.t0, g.t1, g.unroll_eff, lds)
                          : conv_valu_instance(g.t0, g.t1, g.unroll_eff, lds);
@@ -405,7 +421,7 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
 
 int fill_async(float *p, int64_t n, float v, hipStream_t stream) {
     if (n <= 0) return DS_OK;
-    const int64_t blocks = std::min<int64_t>(cdiv64(n, 256), 4096);
+    const int64_t blocks = std::min<int64_t>(cdiv64(cdiv64(n, 4), 256), 2048);
     hipLaunchKernelGGL(fill_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, p, n, v);
     return hip_ok(hipGetLastError(), "fill launch") ? DS_OK : DS_EHIP;
 }

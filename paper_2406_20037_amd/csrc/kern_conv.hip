@@ -26,6 +26,10 @@ namespace ds {
 
 namespace {
 
+__device__ __forceinline__ int fdiv(int n, FastDiv f) {
+    return int((__umulhi(unsigned(n), f.m) + unsigned(n)) >> f.s);
+}
+
 __device__ __forceinline__ void conv_tile_coords(const ConvArgs &a, int &n, int &z, int &kt,
                                                  int &pt, int &qt) {
     int t = xcd_tile(blockIdx.x, gridDim.x);
@@ -47,8 +51,8 @@ __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool ld
     const int RS = a.R * a.S;
     const int real = a.tc * RS;
     for (int e = threadIdx.x; e < a.red; e += blockDim.x) {
-        const int c_l = e / RS, rs = e - c_l * RS;
-        const int r = rs / a.S, s = rs - r * a.S;
+        const int c_l = fdiv(e, a.f_rs), rs = e - c_l * RS;
+        const int r = fdiv(rs, a.f_s), s = rs - r * a.S;
         if (lds) {
             tab[e] = e < real ? c_l * a.hs * a.ws + r * a.ws + s : 0;
         } else {
@@ -60,7 +64,11 @@ __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool ld
     }
 }
 
-// Stage the input halo of chunk c0 and the weights of the tile into LDS.
+// Stage the input halo of chunk c0 and the weights of the tile into LDS.  Each
+// thread issues kBatch independent loads before writing any of them, so the
+// global-load latency is paid once per batch rather than once per element.
+constexpr int kBatch = 8;
+
 __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, int pt, int qt,
                                             int c0, float *wt, float *xs) {
     const int RS = a.R * a.S;
@@ -69,24 +77,51 @@ __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, in
     const int nh = a.tc * hw;
     const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
     const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
-    for (int e = threadIdx.x; e < nh; e += blockDim.x) {
-        const int c_l = e / hw, rem = e - c_l * hw;
-        const int hy = rem / a.ws, hx = rem - hy * a.ws;
-        const int c = c0 + c_l, gy = hy0 + hy, gx = hx0 + hx;
-        float v = 0.f;
-        if (c < a.C && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W)
-            v = xn[((size_t)c * a.H + gy) * a.W + gx];
-        xs[e] = v;
+    const int nt = blockDim.x;
+    for (int e0 = threadIdx.x; e0 < nh; e0 += kBatch * nt) {
+        float v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int e = e0 + u * nt;
+            v[u] = 0.f;
+            if (e < nh) {
+                const int c_l = fdiv(e, a.f_hw), rem = e - c_l * hw;
+                const int hy = fdiv(rem, a.f_ws), hx = rem - hy * a.ws;
+                const int c = c0 + c_l, gy = hy0 + hy, gx = hx0 + hx;
+                if (c < a.C && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W)
+                    v[u] = xn[((size_t)c * a.H + gy) * a.W + gx];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int e = e0 + u * nt;
+            if (e < nh) xs[e] = v[u];
+        }
     }
     if (threadIdx.x == 0) xs[nh] = 0.f;
     const int nw = a.tk * a.red;
     const int crs = a.C * RS;
-    for (int e = threadIdx.x; e < nw; e += blockDim.x) {
-        const int kl = e / a.red, kr = e - kl * a.red;
-        const int k = kt * a.tk + kl;
-        float v = 0.f;
-        if (k < a.K && kr < real && c0 * RS + kr < crs) v = a.w[(size_t)k * crs + c0 * RS + kr];
-        wt[kl * a.wrow + kr] = v;
+    for (int e0 = threadIdx.x; e0 < nw; e0 += kBatch * nt) {
+        float v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int e = e0 + u * nt;
+            v[u] = 0.f;
+            if (e < nw) {
+                const int kl = fdiv(e, a.f_red), kr = e - kl * a.red;
+                const int k = kt * a.tk + kl;
+                if (k < a.K && kr < real && c0 * RS + kr < crs)
+                    v[u] = a.w[(size_t)k * crs + c0 * RS + kr];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int e = e0 + u * nt;
+            if (e < nw) {
+                const int kl = fdiv(e, a.f_red), kr = e - kl * a.red;
+                wt[kl * a.wrow + kr] = v[u];
+            }
+        }
     }
 }
 
@@ -108,7 +143,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
 #pragma unroll
     for (int j = 0; j < PPT; ++j) {
         const int pix = pl + a.npl * j;
-        const int py = pix / a.tw, px = pix - py * a.tw;
+        const int py = pix >> a.ltw, px = pix & (a.tw - 1);
         const int p = pt * a.th + py, q = qt * a.tw + px;
         pv[j] = pix < a.npx && p < a.P && q < a.Q;
         poff[j] = py * a.st * a.ws + px * a.st;
@@ -212,7 +247,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
 #pragma unroll
     for (int b = 0; b < NPB; ++b) {
         const int pix = (wid * NPB + b) * 16 + li;
-        const int py = pix / a.tw, px = pix - py * a.tw;
+        const int py = pix >> a.ltw, px = pix & (a.tw - 1);
         const int p = pt * a.th + py, q = qt * a.tw + px;
         pv[b] = pix < a.npx && p < a.P && q < a.Q;
         poff[b] = py * a.st * a.ws + px * a.st;
