@@ -240,11 +240,14 @@ def conv_geometry(shape, v):
         t0, t1 = tkb, npb           # template parameters: channel blocks, pixel blocks per wave
     hs = (th - 1) * st + R
     ws = (tw - 1) * st + S
+    chunks = max(1, _cdiv(C, tc))
     if v["lds"]:
-        lds = 4 * (tc * hs * ws + 1) + 4 * tk * wrow + 4 * red
+        # weights + halo (+ one zero float) per buffer, rounded to 16 bytes; two
+        # buffers when a workgroup walks more than one chunk; then the table.
+        nbuf = 2 if _cdiv(chunks, v["ks"]) > 1 else 1
+        lds = 4 * (nbuf * _cdiv(tk * wrow + tc * hs * ws + 1, 4) * 4 + red)
     else:
         lds = 8 * red
-    chunks = max(1, _cdiv(C, tc))
     grid = N * v["ks"] * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)
     uf = 1 if v["unroll"] == 0 else min(16, _pow2floor(max(1, v["unroll"] // body)))
     valid = (ok and lds <= LDS_LIMIT and threads <= THREADS_LIMIT and v["ks"] <= chunks

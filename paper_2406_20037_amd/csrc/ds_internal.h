@@ -88,8 +88,9 @@ struct ConvArgs {
     int hs, ws;           // halo tile extent
     int npx, npl;         // pixels per tile, lanes covering pixels (VALU)
     int ltw;              // log2(tw)
-    int atomic;           // 1: accumulate into a zero-filled y
-    FastDiv f_hw, f_ws, f_red, f_rs, f_s;   // divisions by hs*ws, ws, red, R*S, S
+    int nbuf, buf;        // LDS buffers (1 or 2) and floats per buffer (16-byte multiple)
+    float *part;          // ks > 1: split z writes its partial output at part + z * N*K*P*Q
+    FastDiv f_hw, f_ws, f_red, f_rs, f_s, f_wrow;   // divisions by hs*ws, ws, red, R*S, S, wrow
 };
 
 struct MatmulArgs {
@@ -101,7 +102,7 @@ struct MatmulArgs {
     int nkt, kps;         // K-tiles, K-tiles per split
     int vecA, vecB;       // 1: 16-byte loads along K of A / along N of B are legal
     int direct;           // 1: every tile is full and aligned: K-tiles go straight to LDS
-    int atomic;
+    float *part;          // ks > 1: split z writes its partial C at part + z * M*N
 };
 
 struct Plan {
@@ -109,7 +110,7 @@ struct Plan {
     int threads = 0;
     int64_t grid = 0;
     int lds = 0;
-    bool zero_fill = false;   // y must be zeroed first (split reduction)
+    int splits = 1;           // non-empty reduction splits; > 1: partials reduced into y
     int64_t y_elems = 0;
     int op = 0;
     ConvArgs conv{};
@@ -119,6 +120,7 @@ struct Plan {
 // Builds the plan of schedule s for buffers (x, w, y); DS_EINVALID_SCHED if s is
 // not a valid point.
 int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan &plan);
+int attach_workspace(Plan &plan);     // split reductions: library-owned partial buffer
 int launch_plan(const Plan &plan, hipStream_t stream);
 
 // Kernel instance lookup (compiled template instances).

@@ -52,6 +52,29 @@ __global__ void fill_kernel(float *p, int64_t n, float v) {
     if (tid < n - t0) p[t0 + tid] = v;
 }
 
+// y[i] = sum over z < splits of part[z * n + i], summed in split order.
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float *__restrict__ part,
+                                                           float *__restrict__ y, int64_t n,
+                                                           int splits) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    const bool vec = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(y) % 16 == 0) &&
+                     (reinterpret_cast<uintptr_t>(part) % 16 == 0);
+    if (vec) {
+        const int64_t n4 = n / 4;
+        for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n4; i += stride) {
+            floatx4 s = reinterpret_cast<const floatx4 *>(part)[i];
+            for (int z = 1; z < splits; ++z) s += reinterpret_cast<const floatx4 *>(part + z * n)[i];
+            reinterpret_cast<floatx4 *>(y)[i] = s;
+        }
+    } else {
+        for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+            float s = part[i];
+            for (int z = 1; z < splits; ++z) s += part[z * n + i];
+            y[i] = s;
+        }
+    }
+}
+
 __global__ void fill_u32_kernel(unsigned *p, int n) {
     if (int(threadIdx.x) < n) p[threadIdx.x] = 0u;
 }
@@ -127,6 +150,8 @@ constexpr int kMaxDevices = 64;
 std::mutex g_mu;
 unsigned *g_parity_buf[kMaxDevices];     // 4 words per device, library-owned
 hipStream_t g_graph_stream[kMaxDevices];  // capture / replay stream per device
+float *g_split_ws[kMaxDevices];           // partial outputs of split reductions
+int64_t g_split_ws_elems[kMaxDevices];
 std::set<std::pair<int, const void *>> g_lds_attr;
 
 int current_device(int &dev) {
@@ -164,6 +189,31 @@ int graph_stream(hipStream_t *out) {
         g_graph_stream[dev] = st;
     }
     *out = g_graph_stream[dev];
+    return DS_OK;
+}
+
+// The per-device workspace of split reductions, grown to at least `elems`
+// floats (kernels queued earlier on any stream must not still be using it:
+// split-reduction launches on one device are expected to be stream-ordered).
+int split_workspace(int64_t elems, float **out) {
+    int dev;
+    int rc = current_device(dev);
+    if (rc != DS_OK) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_split_ws_elems[dev] < elems) {
+        if (g_split_ws[dev]) {
+            if (!hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize")) return DS_EHIP;
+            (void)hipFree(g_split_ws[dev]);
+            g_split_ws[dev] = nullptr;
+            g_split_ws_elems[dev] = 0;
+        }
+        void *p = nullptr;
+        if (!hip_ok(hipMalloc(&p, size_t(elems) * sizeof(float)), "hipMalloc(split workspace)"))
+            return DS_ENOMEM;
+        g_split_ws[dev] = static_cast<float *>(p);
+        g_split_ws_elems[dev] = elems;
+    }
+    *out = g_split_ws[dev];
     return DS_OK;
 }
 
@@ -388,10 +438,12 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.f_red = make_fastdiv(a.red);
         a.f_rs = make_fastdiv(a.R * a.S);
         a.f_s = make_fastdiv(a.S);
-        a.atomic = a.ks > 1;
+        a.f_wrow = make_fastdiv(a.wrow);
+        a.nbuf = cdiv64(a.chunks, a.ks) > 1 ? 2 : 1;
+        a.buf = int(cdiv64(int64_t(a.tk) * a.wrow + int64_t(a.tc) * a.hs * a.ws + 1, 4) * 4);
         plan.func = mfma ? conv_mfma_instance(g.t0, g.t1, g.unroll_eff, lds)
                          : conv_valu_instance(g.t0, g.t1, g.unroll_eff, lds);
-        plan.zero_fill = a.ks > 1;
+        plan.splits = a.ks > 1 ? int(cdiv64(a.chunks, a.cps)) : 1;
         plan.y_elems = int64_t(a.N) * a.K * a.P * a.Q;
     } else {
         MatmulArgs &a = plan.mm;
@@ -406,16 +458,28 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.vecA = (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
         a.vecB = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
         a.direct = a.vecA && a.vecB && a.M % bm == 0 && a.N % bn == 0 && a.K % bk == 0;
-        a.atomic = a.ks > 1;
         plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf)
                          : mm_valu_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf);
-        plan.zero_fill = a.ks > 1;
+        plan.splits = a.ks > 1 ? int(cdiv64(a.nkt, a.kps)) : 1;
         plan.y_elems = int64_t(a.M) * a.N;
     }
     if (!plan.func) {
         set_error("no compiled kernel instance for this schedule");
         return DS_EUNSUPPORTED;
     }
+    return DS_OK;
+}
+
+int attach_workspace(Plan &plan) {
+    if (plan.splits <= 1 || plan.y_elems == 0 || plan.grid == 0) return DS_OK;
+    // Splits that own no reduction step exit early; the reduce kernel sums only
+    // the first plan.splits partial slices.
+    float *part = nullptr;
+    const int ks = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.ks : plan.mm.ks;
+    const int rc = split_workspace(int64_t(ks) * plan.y_elems, &part);
+    if (rc != DS_OK) return rc;
+    if (plan.op == DS_OP_CONV2D_NCHW) plan.conv.part = part;
+    else plan.mm.part = part;
     return DS_OK;
 }
 
@@ -428,11 +492,6 @@ int fill_async(float *p, int64_t n, float v, hipStream_t stream) {
 
 int launch_plan(const Plan &plan, hipStream_t stream) {
     if (plan.grid == 0 || plan.y_elems == 0) return DS_OK;
-    float *y = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.y : plan.mm.C;
-    if (plan.zero_fill) {
-        const int rc = fill_async(y, plan.y_elems, 0.f, stream);
-        if (rc != DS_OK) return rc;
-    }
     int rc = ensure_lds_attr(plan.func, plan.lds);
     if (rc != DS_OK) return rc;
     void *args[1];
@@ -442,6 +501,15 @@ int launch_plan(const Plan &plan, hipStream_t stream) {
                                 size_t(plan.lds), stream),
                 "hipLaunchKernel"))
         return DS_EHIP;
+    if (plan.splits > 1) {
+        float *y = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.y : plan.mm.C;
+        const float *part = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.part : plan.mm.part;
+        const int64_t n4 = cdiv64(plan.y_elems, 4);
+        const int64_t blocks = std::min<int64_t>(cdiv64(n4, 256), 4096);
+        hipLaunchKernelGGL(split_reduce_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, part, y,
+                           plan.y_elems, plan.splits);
+        if (!hip_ok(hipGetLastError(), "split reduce launch")) return DS_EHIP;
+    }
     return DS_OK;
 }
 
@@ -491,6 +559,8 @@ int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float 
         set_error("null buffer");
         return DS_EINVAL;
     }
+    rc = attach_workspace(plan);
+    if (rc != DS_OK) return rc;
     return launch_plan(plan, stream);
 }
 
@@ -586,6 +656,11 @@ int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cf
     if (plan.y_elems > 0 && (!io->x || !io->w || !io->y)) {
         set_error("null buffer");
         return DS_EINVAL;
+    }
+    rc = attach_workspace(plan);
+    if (rc != DS_OK) {
+        out->status = rc;
+        return DS_OK;
     }
     const hipStream_t stream = io->stream;
     const bool check = cfg.check && io->ref && plan.y_elems > 0;
@@ -763,13 +838,17 @@ void ds_shutdown(void) {
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return;
     for (int d = 0; d < kMaxDevices; ++d) {
-        if (!g_parity_buf[d] && !g_graph_stream[d]) continue;
+        if (!g_parity_buf[d] && !g_graph_stream[d] && !g_split_ws[d]) continue;
         if (hipSetDevice(d) == hipSuccess) {
+            (void)hipDeviceSynchronize();
             if (g_parity_buf[d]) (void)hipFree(g_parity_buf[d]);
             if (g_graph_stream[d]) (void)hipStreamDestroy(g_graph_stream[d]);
+            if (g_split_ws[d]) (void)hipFree(g_split_ws[d]);
         }
         g_parity_buf[d] = nullptr;
         g_graph_stream[d] = nullptr;
+        g_split_ws[d] = nullptr;
+        g_split_ws_elems[d] = 0;
     }
     (void)hipSetDevice(cur);
     g_lds_attr.clear();

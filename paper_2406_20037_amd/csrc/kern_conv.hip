@@ -14,10 +14,13 @@
 //              wave holds TKB x NPB 16x16 blocks.  Lane group g (lanes
 //              16g..16g+15) feeds reduction steps kr = 16*j + 4*g + v, v < 4,
 //              for both operands, so a 16-byte LDS read gives four steps of A.
+//              Operands of the next 16-step group are read while the MFMAs of
+//              the current one run.
 //
 // LDS layout (lds=1): [weights tk x wrow][input halo tc x hs x ws][zero][table red]
 //             (lds=0): [table red x {offset, info}]
-// A split (ks > 1) accumulates with atomics into a zero-filled y.
+// A split (ks > 1) stores its partial output tile; a reduce kernel sums the
+// splits into y in split order.
 #include <utility>
 
 #include "kern_common.h"
@@ -62,6 +65,15 @@ __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool ld
                                       : 0;
         }
     }
+}
+
+// Offset (within one output channel's weights) of staged reduction index kr of
+// the chunk starting at channel c0; false if kr reads zero.
+__device__ __forceinline__ bool weight_src(const ConvArgs &a, int kr, int c0, int real, int crs,
+                                           int &gofs) {
+    const int RS = a.R * a.S;
+    gofs = c0 * RS + kr;
+    return kr < real && gofs < crs;
 }
 
 // Stage the input halo of chunk c0 and the weights of the tile into LDS.  Each
@@ -110,8 +122,9 @@ __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, in
             if (e < nw) {
                 const int kl = fdiv(e, a.f_red), kr = e - kl * a.red;
                 const int k = kt * a.tk + kl;
-                if (k < a.K && kr < real && c0 * RS + kr < crs)
-                    v[u] = a.w[(size_t)k * crs + c0 * RS + kr];
+                int gofs;
+                if (weight_src(a, kr, c0, real, crs, gofs) && k < a.K)
+                    v[u] = a.w[(size_t)k * crs + gofs];
             }
         }
 #pragma unroll
@@ -123,6 +136,73 @@ __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, in
             }
         }
     }
+}
+
+#define DS_GLOBAL(p) ((const __attribute__((address_space(1))) void *)(p))
+#define DS_LOCAL(p) ((__attribute__((address_space(3))) void *)(p))
+
+// The same staging as stage_chunk, issued as asynchronous global -> LDS copies
+// (4 bytes per lane; a wave's instruction fills 64 consecutive LDS floats);
+// positions that read zero (padding, channels past C, reduction padding) are
+// written with ordinary LDS stores.  Needs a whole number of waves.
+__device__ __forceinline__ void dma_chunk(const ConvArgs &a, int n, int kt, int pt, int qt, int c0,
+                                          float *wt, float *xs) {
+    const int RS = a.R * a.S;
+    const int real = a.tc * RS;
+    const int crs = a.C * RS;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nwv = blockDim.x >> 6;
+    const int npw = a.tk * a.wrow;
+    for (int base = wid * 64; base < npw; base += nwv * 64) {
+        const int p = base + lane;
+        if (p < npw) {
+            const int kl = fdiv(p, a.f_wrow), kr = p - kl * a.wrow;
+            const int k = kt * a.tk + kl;
+            int gofs;
+            if (kr < a.red && weight_src(a, kr, c0, real, crs, gofs) && k < a.K)
+                __builtin_amdgcn_global_load_lds(DS_GLOBAL(a.w + (size_t)k * crs + gofs),
+                                                 DS_LOCAL(wt + base), 4, 0, 0);
+            else if (kr < a.red)
+                wt[p] = 0.f;
+        }
+    }
+    const int hw = a.hs * a.ws;
+    const int nh = a.tc * hw;
+    const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
+    const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
+    for (int base = wid * 64; base < nh; base += nwv * 64) {
+        const int p = base + lane;
+        if (p < nh) {
+            const int c_l = fdiv(p, a.f_hw), rem = p - c_l * hw;
+            const int hy = fdiv(rem, a.f_ws), hx = rem - hy * a.ws;
+            const int c = c0 + c_l, gy = hy0 + hy, gx = hx0 + hx;
+            if (c < a.C && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W)
+                __builtin_amdgcn_global_load_lds(
+                    DS_GLOBAL(xn + ((size_t)c * a.H + gy) * a.W + gx), DS_LOCAL(xs + base), 4, 0, 0);
+            else
+                xs[p] = 0.f;
+        }
+    }
+    if (threadIdx.x == 0) xs[nh] = 0.f;
+}
+
+// Waits for this wave's outstanding copies and LDS operations, then barriers
+// the workgroup (no memory fence: the waits make every wave's LDS writes
+// complete before any wave passes).
+__device__ __forceinline__ void chunk_barrier() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Stages chunk ci of this workgroup into LDS buffer b.
+__device__ __forceinline__ void stage_to(const ConvArgs &a, float *smem, int b, int n, int kt, int pt,
+                                         int qt, int ci) {
+    float *wt = smem + b * a.buf;
+    float *xs = wt + a.tk * a.wrow;
+    if ((blockDim.x & 63) == 0) dma_chunk(a, n, kt, pt, qt, ci * a.tc, wt, xs);
+    else stage_chunk(a, n, kt, pt, qt, ci * a.tc, wt, xs);
 }
 
 template <int KPT, int PPT, int UF, int LDS>
@@ -158,20 +238,20 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
 #pragma unroll
         for (int j = 0; j < PPT; ++j) acc[i][j] = 0.f;
 
-    float *wt = smem;
-    float *xs = smem + a.tk * a.wrow;
-    int *tab = LDS ? reinterpret_cast<int *>(xs + a.tc * a.hs * a.ws + 1)
-                   : reinterpret_cast<int *>(smem);
+    int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
     build_table(a, tab, LDS);
+    if (LDS) stage_to(a, smem, 0, n, kt, pt, qt, ci0);
 
     const int RS = a.R * a.S;
     const int crs = a.C * RS;
     for (int ci = ci0; ci < ci1; ++ci) {
         const int c0 = ci * a.tc;
         if (LDS) {
-            __syncthreads();
-            stage_chunk(a, n, kt, pt, qt, c0, wt, xs);
-            __syncthreads();
+            const int bi = (ci - ci0) & 1;
+            chunk_barrier();
+            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1);
+            const float *wt = smem + bi * a.buf;
+            const float *xs = wt + a.tk * a.wrow;
             const float *wg = wt + g * KPT * a.wrow;
 #pragma unroll UF
             for (int kr = 0; kr < a.red; ++kr) {
@@ -214,18 +294,14 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         }
     }
 
-    float *yn = a.y + (size_t)n * a.K * PQ;
+    float *yn = (a.ks > 1 ? a.part + (size_t)z * a.N * a.K * PQ : a.y) + (size_t)n * a.K * PQ;
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
         const int k = k0 + i;
         if (k >= a.K) continue;
 #pragma unroll
-        for (int j = 0; j < PPT; ++j) {
-            if (!pv[j]) continue;
-            float *dst = yn + (size_t)k * PQ + oq[j];
-            if (a.atomic) atomicAdd(dst, acc[i][j]);
-            else *dst = acc[i][j];
-        }
+        for (int j = 0; j < PPT; ++j)
+            if (pv[j]) yn[(size_t)k * PQ + oq[j]] = acc[i][j];
     }
 }
 
@@ -262,11 +338,9 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
 #pragma unroll
         for (int b = 0; b < NPB; ++b) acc[i][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    float *wt = smem;
-    float *xs = smem + a.tk * a.wrow;
-    int *tab = LDS ? reinterpret_cast<int *>(xs + a.tc * a.hs * a.ws + 1)
-                   : reinterpret_cast<int *>(smem);
+    int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
     build_table(a, tab, LDS);
+    if (LDS) stage_to(a, smem, 0, n, kt, pt, qt, ci0);
 
     constexpr int UG = UF >= 4 ? UF / 4 : 1;   // 16-step groups unrolled
     const int RS = a.R * a.S;
@@ -275,28 +349,49 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
     for (int ci = ci0; ci < ci1; ++ci) {
         const int c0 = ci * a.tc;
         if (LDS) {
-            __syncthreads();
-            stage_chunk(a, n, kt, pt, qt, c0, wt, xs);
-            __syncthreads();
-#pragma unroll UG
-            for (int kg = 0; kg < ngroups; ++kg) {
-                const int kb = kg * 16 + 4 * lg;
-                floatx4 av[TKB];
+            const int bi = (ci - ci0) & 1;
+            chunk_barrier();
+            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1);
+            const float *wt = smem + bi * a.buf;
+            const float *xs = wt + a.tk * a.wrow;
+            {
+                // Two groups per iteration with two named operand sets: the
+                // reads of group kg+1 are issued before the MFMAs of group kg
+                // (LDS returns in order, so those MFMAs need not wait for them).
+                auto load = [&](int kg, floatx4 (&av)[TKB], float (&bv)[4][NPB]) {
+                    const int kb = kg * 16 + 4 * lg;
+                    int off[4];
 #pragma unroll
-                for (int i = 0; i < TKB; ++i)
-                    av[i] = *reinterpret_cast<const floatx4 *>(wt + (i * 16 + li) * a.wrow + kb);
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int off = tab[kb + v];
-                    float bv[NPB];
-#pragma unroll
-                    for (int b = 0; b < NPB; ++b) bv[b] = xs[off + poff[b]];
+                    for (int v = 0; v < 4; ++v) off[v] = tab[kb + v];
 #pragma unroll
                     for (int i = 0; i < TKB; ++i)
+                        av[i] = *reinterpret_cast<const floatx4 *>(wt + (i * 16 + li) * a.wrow + kb);
 #pragma unroll
-                        for (int b = 0; b < NPB; ++b)
-                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][v], bv[b],
-                                                                            acc[i][b], 0, 0, 0);
+                    for (int v = 0; v < 4; ++v)
+#pragma unroll
+                        for (int b = 0; b < NPB; ++b) bv[v][b] = xs[off[v] + poff[b]];
+                };
+                auto mma = [&](const floatx4 (&av)[TKB], const float (&bv)[4][NPB]) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+#pragma unroll
+                        for (int i = 0; i < TKB; ++i)
+#pragma unroll
+                            for (int b = 0; b < NPB; ++b)
+                                acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                    av[i][v], bv[v][b], acc[i][b], 0, 0, 0);
+                };
+                floatx4 a0[TKB], a1[TKB];
+                float b0[4][NPB], b1[4][NPB];
+                load(0, a0, b0);
+                for (int kg = 0; kg < ngroups; kg += 2) {
+                    const bool two = kg + 1 < ngroups;
+                    if (two) load(kg + 1, a1, b1);
+                    mma(a0, b0);
+                    if (two) {
+                        if (kg + 2 < ngroups) load(kg + 2, a0, b0);
+                        mma(a1, b1);
+                    }
                 }
             }
         } else {
@@ -338,7 +433,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
     }
 
     // 16x16 block: lane holds rows 4*lg + v (channels), column li (pixel).
-    float *yn = a.y + (size_t)n * a.K * PQ;
+    float *yn = (a.ks > 1 ? a.part + (size_t)z * a.N * a.K * PQ : a.y) + (size_t)n * a.K * PQ;
 #pragma unroll
     for (int i = 0; i < TKB; ++i)
 #pragma unroll
@@ -347,10 +442,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int k = kt * a.tk + i * 16 + 4 * lg + v;
-                if (k >= a.K) continue;
-                float *dst = yn + (size_t)k * PQ + oq[b];
-                if (a.atomic) atomicAdd(dst, acc[i][b][v]);
-                else *dst = acc[i][b][v];
+                if (k < a.K) yn[(size_t)k * PQ + oq[b]] = acc[i][b][v];
             }
         }
 }

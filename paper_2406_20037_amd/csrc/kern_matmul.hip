@@ -20,7 +20,8 @@
 //            v_mfma_f32_16x16x4f32).  Lane group g feeds k = kk + VEC*g + v
 //            (v < VEC) to both operands, so one VEC-wide LDS read of A serves
 //            VEC MFMA steps.
-// A split (ks > 1) accumulates with atomics into a zero-filled C.
+// A split (ks > 1) stores its partial C tile; a reduce kernel sums the splits
+// into C in split order.
 #include <utility>
 
 #include "kern_common.h"
@@ -269,17 +270,16 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
     };
     k_loop<BM, BN, BK, DB>(a, m0, n0, kt0, kt1, smem, compute);
 
+    float *cbase = a.ks > 1 ? a.part + (size_t)z * a.M * a.N : a.C;
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
         const int gm = m0 + ty * RM + i;
         if (gm >= a.M) continue;
-        float *crow = a.C + (size_t)gm * a.N;
+        float *crow = cbase + (size_t)gm * a.N;
 #pragma unroll
         for (int j = 0; j < RN; ++j) {
             const int gn = n0 + tx * RN + j;
-            if (gn >= a.N) continue;
-            if (a.atomic) atomicAdd(crow + gn, acc[i][j]);
-            else crow[gn] = acc[i][j];
+            if (gn < a.N) crow[gn] = acc[i][j];
         }
     }
 }
@@ -358,6 +358,7 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
 
     // Output layout: 32x32 block, lane holds rows 8*(v/4) + 4*lg + v%4 of
     // column li (v < 16); 16x16 block, rows 4*lg + v of column li (v < 4).
+    float *cbase = a.ks > 1 ? a.part + (size_t)z * a.M * a.N : a.C;
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -370,9 +371,7 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
                 const int row = BIG ? 8 * (v / 4) + 4 * lg + (v % 4) : 4 * lg + v;
                 const int gm = m0 + wr * WM + i * IM + row;
                 if (gm >= a.M) continue;
-                float *dst = a.C + (size_t)gm * a.N + gn;
-                if (a.atomic) atomicAdd(dst, acc[i][j][v]);
-                else *dst = acc[i][j][v];
+                cbase[(size_t)gm * a.N + gn] = acc[i][j][v];
             }
         }
 }

@@ -108,13 +108,18 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         g.t1 = npb;
     }
     const int64_t hs = int64_t(th - 1) * st + R, ws = int64_t(tw - 1) * st + S;
-    int64_t lds_bytes;
-    if (lds)
-        lds_bytes = 4 * (tc * hs * ws + 1) + 4 * int64_t(tk) * wrow + 4 * int64_t(g.red);
-    else
-        lds_bytes = 8 * int64_t(g.red);
-    g.lds_bytes = int(std::min<int64_t>(lds_bytes, INT32_MAX));
     g.chunks = std::max<int64_t>(1, cdiv(C, tc));
+    int64_t lds_bytes;
+    if (lds) {
+        // Two buffers (weights + halo + a zero float, 16-byte rounded) when a
+        // workgroup walks more than one chunk, then the offset table.
+        const int64_t nbuf = cdiv(g.chunks, ks) > 1 ? 2 : 1;
+        const int64_t buf = cdiv(int64_t(tk) * wrow + tc * hs * ws + 1, 4) * 4;
+        lds_bytes = 4 * (nbuf * buf + int64_t(g.red));
+    } else {
+        lds_bytes = 8 * int64_t(g.red);
+    }
+    g.lds_bytes = int(std::min<int64_t>(lds_bytes, INT32_MAX));
     g.grid = N * ks * cdiv(K, tk) * cdiv(P, th) * cdiv(Q, tw);
     g.unroll_eff = unroll == 0 ? 1 : std::min(16, pow2_floor(std::max(1, unroll / body)));
     g.valid = ok && lds_bytes <= kLdsLimit && g.threads <= kThreadsLimit && ks <= g.chunks &&

@@ -78,30 +78,34 @@ def test_conv_geometry_hand_computed():
     g = s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1))
     # 64 pixels -> one 16-pixel block per wave; 16 channels -> one block.
     # reduction 16*9 = 144; halo 10x10; LDS 4*(16*100+1) + 4*16*144 + 4*144.
-    # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148.
-    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256, lds_bytes=16452, acc=4,
+    # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148; 4 chunks
+    # in one split -> two buffers of 16*148 + 16*100 + 1 -> 3972 floats, + table.
+    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256, lds_bytes=4 * (2 * 3972 + 144), acc=4,
                      unroll_eff=16, t0=1, t1=1, red=144, chunks=4)
     g = s.geometry(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0))
     # 128 pixels x 4 channels -> 256 threads, 2 channel groups of 2; unroll 16//2 = 8.
     assert g == dict(valid=True, grid=2 * 16 * 14 * 2, threads=256, lds_bytes=8 * 72, acc=2,
                      unroll_eff=8, t0=2, t1=1, red=72, chunks=8)
-    # One pixel, 64 channels: one wave, one channel per lane.
+    # One pixel, 64 channels: one wave, one channel per lane; 32 chunks -> two
+    # buffers of 64*18 + 2*3*3 + 1 = 1171 -> 1172 floats, + table.
     g = s.geometry(idx_of(s, tk=64, th=1, tw=1, tc=2, unroll=0, lds=1, ks=1, mfma=0))
-    assert g == dict(valid=True, grid=56 * 56, threads=64, lds_bytes=4 * (2 * 9 + 1) + 4 * 64 * 18
-                     + 4 * 18, acc=1, unroll_eff=1, t0=1, t1=1, red=18, chunks=32)
+    assert g == dict(valid=True, grid=56 * 56, threads=64, lds_bytes=4 * (2 * 1172 + 18),
+                     acc=1, unroll_eff=1, t0=1, t1=1, red=18, chunks=32)
     # Fewer than 64 outputs: not a full wave.
     assert not s.valid(idx_of(s, tk=2, th=4, tw=4, tc=1, unroll=0, lds=0, ks=1, mfma=0))
-    # MFMA reduction padded to a multiple of 16: 4 channels x 9 taps = 36 -> 48.
+    # MFMA reduction padded to a multiple of 16: 4 channels x 9 taps = 36 -> 48;
+    # 16 chunks -> two buffers of 32*52 + 4*6*18 + 1 = 2097 -> 2100 floats.
     g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1))
-    assert g["red"] == 48 and g["lds_bytes"] == 4 * (4 * 6 * 18 + 1) + 4 * 32 * 52 + 4 * 48
+    assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2100 + 48)
     # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
     assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
     # MFMA needs >= 16 channels and >= 64 pixels.
     assert not s.valid(idx_of(s, tk=8, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
     assert not s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
-    # LDS limit: 64-channel chunk of a 34x34 halo does not fit.
+    # LDS limit: 64-channel chunk of a 34x34 halo does not fit (one chunk, one
+    # buffer of 16*576 + 64*34*34 + 1 -> 83204 floats).
     g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0))
-    assert g["lds_bytes"] == 4 * (64 * 34 * 34 + 1) + 4 * 16 * 576 + 4 * 576 and not g["valid"]
+    assert g["lds_bytes"] == 4 * (83204 + 576) and not g["valid"]
     # split finer than the chunk count.
     assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0))
 
