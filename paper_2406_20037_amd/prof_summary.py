@@ -12,10 +12,30 @@ from __future__ import annotations
 
 import argparse
 import collections
+import hashlib
+import json
+import os
 import sqlite3
 import sys
 
 COPY = "__amd_rocclr_copyBuffer"
+PKG = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = {
+    "mm_": ["csrc/kern_matmul.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
+    "conv_": ["csrc/kern_conv.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
+}
+
+
+def source_hash(kernel: str) -> str | None:
+    """sha256 over the source files a kernel family is compiled from."""
+    for prefix, files in KERNEL_SOURCES.items():
+        if kernel.startswith(prefix):
+            h = hashlib.sha256()
+            for f in files:
+                with open(os.path.join(PKG, f), "rb") as fh:
+                    h.update(fh.read())
+            return h.hexdigest()
+    return None
 
 
 def short(name: str) -> str:
@@ -47,6 +67,10 @@ def main(argv=None):
     ap.add_argument("--write")
     ap.add_argument("--copy-mib", type=int, default=64)
     ap.add_argument("--top", type=int, default=15)
+    ap.add_argument("--counters", nargs="*", default=[],
+                    help="further --pmc runs: every counter per kernel (mean per dispatch)")
+    ap.add_argument("--json-out", help="merge the scaled HBM bytes of our kernels into this file")
+    ap.add_argument("--command", default="", help="recorded with the --json-out entries")
     args = ap.parse_args(argv)
     rows, n = top_kernels(args.trace, args.top)
     print(f"### Kernel trace ({n} distinct kernels; top {len(rows)} by total time)\n")
@@ -69,11 +93,36 @@ def main(argv=None):
               "write bytes (scaled) |")
         print("|---|---:|---:|---:|---:|---:|")
         names = sorted({k[0] for k in f} | {k[0] for k in w})
+        entries = {}
         for name in names:
             fv = f.get((name, "FETCH_SIZE"), float("nan"))
             wv = w.get((name, "WRITE_SIZE"), float("nan"))
             print(f"| `{short(name)}` | {fn.get((name, 'FETCH_SIZE'), 0)} | {fv:.1f} | {wv:.1f} | "
                   f"{fv * ff * 1024:.0f} | {wv * wf * 1024:.0f} |")
+            k = short(name)
+            sh = source_hash(k)
+            if sh:
+                entries[k] = {"fetch_kib": fv, "write_kib": wv, "read_factor": ff,
+                              "write_factor": wf, "read_bytes": fv * ff * 1024,
+                              "write_bytes": wv * wf * 1024, "source_sha256": sh,
+                              "command": args.command}
+        if args.json_out and entries:
+            data = {}
+            if os.path.exists(args.json_out):
+                with open(args.json_out) as fh:
+                    data = json.load(fh)
+            data.update(entries)
+            with open(args.json_out, "w") as fh:
+                json.dump(data, fh, indent=1, sort_keys=True)
+    for db in args.counters:
+        c, cn = counters(db)
+        names = sorted({k[1] for k in c})
+        print(f"\n### Counters ({', '.join(names)}; mean per dispatch)\n")
+        print("| kernel | dispatches | " + " | ".join(names) + " |")
+        print("|---|---:|" + "---:|" * len(names))
+        for k in sorted({k[0] for k in c}):
+            vals = " | ".join(f"{c.get((k, n), float('nan')):.4g}" for n in names)
+            print(f"| `{short(k)}` | {cn.get((k, names[0]), 0)} | {vals} |")
     return 0
 
 
