@@ -13,6 +13,10 @@ Contents:
 * ``sampler``  -- the seeded exploration sampler (own SplitMix64).
 * ``droplet``  -- Droplet Search coordinate descent and the combined
   explore-then-exploit procedure, plus the rank-sum convergence test.
+* ``exploiters`` -- the strategies Droplet Search is compared with as the
+  exploitation phase (Random, Grid, GA; Section 3, RQ4).
+* ``task_scheduler`` -- one trial budget split across the layers of a network
+  (Section 2.1, Termination in Ansor), then Droplet Search per layer.
 
 Parity status of each part is stated in its module header.
 """
