@@ -304,6 +304,112 @@ int droplet_tune_ex(const ds_space *space, const ds_sched *start, int budget,
 int ds_tune(const ds_space *space, const ds_tune_cfg *cfg, const ds_tune_io *io,
             ds_measure_fn fn, void *ctx, ds_tune_result *res, ds_trace *trace);
 
+/* ---- measurement cache, exploration, exploitation strategies --------------- */
+
+/*
+ * ds_cache -- the measurements of one space, keyed by lattice key (opaque,
+ * library-owned until ds_cache_destroy).  Exploration fills it; every
+ * exploitation strategy skips points it holds and adds what it measures, so
+ * several strategies can start from one exploration (Section 3, RQ4: each
+ * technique exploits the same best exploration sample).  A cache is bound to
+ * the space it was created for (same op, shape and axes).
+ */
+typedef struct ds_cache ds_cache;
+
+int ds_cache_create(const ds_space *space, ds_cache **out);
+void ds_cache_destroy(ds_cache *cache);
+/* Deep copy (so each strategy starts from the same exploration state). */
+int ds_cache_clone(const ds_cache *cache, ds_cache **out);
+/* Number of cached points (>= 0) or a negative status. */
+int ds_cache_size(const ds_cache *cache);
+/* 1 and *out filled if s is cached, 0 if not, < 0 on error. */
+int ds_cache_get(const ds_cache *cache, const ds_sched *s, ds_measurement *out);
+
+/*
+ * ds_explore -- a2 alone: draw cfg->n_explore points (as ansor_draw with
+ * cfg->seed) and measure each into cache; a point already cached keeps its
+ * measurement and is not measured again.  res->seed_point / seed_ms (and
+ * best / best_ms) are the fastest drawn point (ties: first drawn);
+ * n_explore_measured counts new measurements; n_failed and explore_s are
+ * filled.  DS_EEXHAUSTED if nothing can be drawn.
+ */
+int ds_explore(const ds_space *space, const ds_tune_cfg *cfg, const ds_tune_io *io,
+               ds_measure_fn fn, void *ctx, ds_cache *cache, ds_tune_result *res,
+               ds_trace *trace);
+
+/* Exploitation strategies compared in Section 3, RQ4. */
+enum {
+    DS_EXPLOIT_DROPLET = 0,  /* Droplet Search (Section 2.2): converges, at most budget trials */
+    DS_EXPLOIT_RANDOM = 1,   /* independent uniform draws of each axis index */
+    DS_EXPLOIT_GRID = 2,     /* mixed-radix walk key(start)+1, +2, ... (first axis fastest) */
+    DS_EXPLOIT_GA = 3        /* genetic algorithm: elitism, roulette selection by 1/time,
+                                one-point crossover, per-gene mutation */
+};
+
+typedef struct {
+    int32_t kind;          /* DS_EXPLOIT_* */
+    int32_t budget;        /* charged trials (100, Section 3 RQ4) */
+    uint64_t seed;         /* SplitMix64 stream of Random and GA */
+    int32_t valid_only;    /* 0: an invalid candidate is a failed trial that costs one
+                              trial, as in the paper's host framework (default);
+                              1: invalid candidates are skipped without charge.
+                              Droplet visits valid neighbours only, either way. */
+    int32_t pop;           /* GA population (20; >= 2) */
+    int32_t elite;         /* GA elites kept per generation (3; 0 <= elite < pop) */
+    double mutation;       /* GA per-gene mutation probability (0.1) */
+} ds_exploit_cfg;
+
+void ds_exploit_cfg_default(ds_exploit_cfg *cfg);
+
+/*
+ * ds_exploit -- run one strategy from start (must be a valid point).  The start
+ * is measured (not charged) unless cached.  Random, Grid and GA skip cached
+ * candidates without charge, stop after cfg->budget charged trials or when
+ * their candidate stream ends (Random: 100*budget draws; Grid: back at the
+ * start; GA: neither crossover nor the Random stream yields a new point), and
+ * return the fastest of the start and their trials (ties: earliest).
+ * tcfg supplies alpha, frozen_mask (Droplet) and the measurement settings.
+ * cache may be NULL (a private one is used).  res->n_droplet_measured counts
+ * the strategy's measurements (start included when measured), res->n_failed
+ * its failed trials, res->droplet_s its wall-clock.  Trace stages: 1 start,
+ * 2 trial.
+ */
+int ds_exploit(const ds_space *space, const ds_sched *start, const ds_exploit_cfg *cfg,
+               const ds_tune_cfg *tcfg, const ds_tune_io *io, ds_measure_fn fn, void *ctx,
+               ds_cache *cache, ds_tune_result *res, ds_trace *trace);
+
+/* One kernel (task) of a network for ds_tune_tasks. */
+typedef struct {
+    const ds_space *space;
+    ds_tune_io io;         /* GPU buffers of this task (used when fn is NULL) */
+    ds_measure_fn fn;      /* NULL: measure on the GPU; else fn(ctx, ...) */
+    void *ctx;
+    double weight;         /* occurrences of the kernel in the network */
+    uint64_t seed;         /* this task's exploration stream */
+} ds_task;
+
+typedef struct {
+    int32_t task;
+    int32_t trials;
+} ds_round;
+
+/*
+ * ds_tune_tasks -- one exploration budget for a whole network (Section 2.1,
+ * Termination in Ansor; Section 3 setup): each task first receives
+ * q = max(1, min(total_trials / n_tasks, 64)) trials in task order; while fewer
+ * than total_trials were spent, the live task with the largest weight *
+ * best time (ties: lowest index) receives min(q, total_trials - spent) more; a
+ * task whose stream ends leaves the worklist.  A task's trials are the next
+ * points of its sampler stream (the first n of ansor_draw(seed, n)).  Then
+ * Droplet Search runs per task from its best sample with cfg->budget and
+ * cfg->alpha.  results[t] holds task t's outcome; rounds (nullable, cap
+ * rounds_cap) the allocation order; *n_rounds the number of rounds;
+ * *network_ms = sum(weight * best_ms).
+ */
+int ds_tune_tasks(const ds_task *tasks, int n_tasks, int total_trials, const ds_tune_cfg *cfg,
+                  ds_tune_result *results, ds_round *rounds, int rounds_cap, int *n_rounds,
+                  double *network_ms);
+
 /*
  * droplet_tune -- the four-argument form: builds the space, allocates seeded
  * U[-1,1) inputs on the current device (SplitMix64 streams 240620037 for x / A

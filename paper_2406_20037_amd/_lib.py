@@ -104,6 +104,24 @@ class ds_trace(C.Structure):
 
 ds_measure_fn = C.CFUNCTYPE(C.c_int, C.c_void_p, C.POINTER(ds_sched), C.POINTER(ds_measurement))
 
+
+class ds_exploit_cfg(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("budget", C.c_int32), ("seed", C.c_uint64),
+                ("valid_only", C.c_int32), ("pop", C.c_int32), ("elite", C.c_int32),
+                ("mutation", C.c_double)]
+
+
+class ds_task(C.Structure):
+    _fields_ = [("space", C.c_void_p), ("io", ds_tune_io), ("fn", ds_measure_fn),
+                ("ctx", C.c_void_p), ("weight", C.c_double), ("seed", C.c_uint64)]
+
+
+class ds_round(C.Structure):
+    _fields_ = [("task", C.c_int32), ("trials", C.c_int32)]
+
+
+DS_EXPLOIT_DROPLET, DS_EXPLOIT_RANDOM, DS_EXPLOIT_GRID, DS_EXPLOIT_GA = 0, 1, 2, 3
+
 # name -> (restype, argtypes); the list is also the set of exported symbols
 SIGNATURES = {
     "sched_space_create": (C.c_int, [C.c_int, C.POINTER(C.c_int64), C.c_int, C.POINTER(C.c_void_p)]),
@@ -142,6 +160,22 @@ SIGNATURES = {
                                   C.POINTER(ds_tune_result), C.POINTER(ds_trace)]),
     "ds_tune": (C.c_int, [C.c_void_p, C.POINTER(ds_tune_cfg), C.POINTER(ds_tune_io), ds_measure_fn,
                           C.c_void_p, C.POINTER(ds_tune_result), C.POINTER(ds_trace)]),
+    "ds_cache_create": (C.c_int, [C.c_void_p, C.POINTER(C.c_void_p)]),
+    "ds_cache_destroy": (None, [C.c_void_p]),
+    "ds_cache_clone": (C.c_int, [C.c_void_p, C.POINTER(C.c_void_p)]),
+    "ds_cache_size": (C.c_int, [C.c_void_p]),
+    "ds_cache_get": (C.c_int, [C.c_void_p, C.POINTER(ds_sched), C.POINTER(ds_measurement)]),
+    "ds_explore": (C.c_int, [C.c_void_p, C.POINTER(ds_tune_cfg), C.POINTER(ds_tune_io),
+                             ds_measure_fn, C.c_void_p, C.c_void_p, C.POINTER(ds_tune_result),
+                             C.POINTER(ds_trace)]),
+    "ds_exploit_cfg_default": (None, [C.POINTER(ds_exploit_cfg)]),
+    "ds_exploit": (C.c_int, [C.c_void_p, C.POINTER(ds_sched), C.POINTER(ds_exploit_cfg),
+                             C.POINTER(ds_tune_cfg), C.POINTER(ds_tune_io), ds_measure_fn,
+                             C.c_void_p, C.c_void_p, C.POINTER(ds_tune_result),
+                             C.POINTER(ds_trace)]),
+    "ds_tune_tasks": (C.c_int, [C.POINTER(ds_task), C.c_int, C.c_int, C.POINTER(ds_tune_cfg),
+                                C.POINTER(ds_tune_result), C.POINTER(ds_round), C.c_int,
+                                C.POINTER(C.c_int), C.POINTER(C.c_double)]),
     "droplet_tune": (C.c_int, [C.c_int, C.POINTER(C.c_int64), C.POINTER(ds_sched), C.c_int,
                                C.POINTER(ds_sched), C.POINTER(C.c_double)]),
     "ds_last_error": (C.c_char_p, []),
@@ -420,6 +454,101 @@ def ds_tune(space, cfg=None, io=None, cost=None, trace_cap=0):
                                  C.byref(tr) if tr else None))
     del keep
     return res, _trace_list(arr, tr)
+
+
+def exploit_cfg(**kw):
+    cfg = ds_exploit_cfg()
+    lib.ds_exploit_cfg_default(C.byref(cfg))
+    for k, v in kw.items():
+        setattr(cfg, k, v)
+    return cfg
+
+
+class Cache:
+    """Owns a ds_cache of one space."""
+
+    def __init__(self, space, _handle=None):
+        self.space = space
+        self.h = C.c_void_p(_handle) if _handle else C.c_void_p()
+        if not _handle:
+            check("ds_cache_create", lib.ds_cache_create(space.h, C.byref(self.h)))
+
+    def __del__(self):
+        try:
+            if self.h:
+                lib.ds_cache_destroy(self.h)
+                self.h = C.c_void_p()
+        except Exception:
+            pass
+
+    def clone(self):
+        h = C.c_void_p()
+        check("ds_cache_clone", lib.ds_cache_clone(self.h, C.byref(h)))
+        return Cache(self.space, h.value)
+
+    def __len__(self):
+        n = lib.ds_cache_size(self.h)
+        check("ds_cache_size", min(n, 0))
+        return n
+
+    def get(self, idx):
+        """The cached ds_measurement of idx, or None."""
+        m = ds_measurement()
+        s = self.space.sched(idx) if not isinstance(idx, ds_sched) else idx
+        rc = lib.ds_cache_get(self.h, C.byref(s), C.byref(m))
+        check("ds_cache_get", min(rc, 0))
+        return m if rc == 1 else None
+
+
+def ds_explore(space, cache, cfg=None, io=None, cost=None, trace_cap=0):
+    res = ds_tune_result()
+    arr, tr = _trace(trace_cap)
+    cb, keep = _callback(cost)
+    check("ds_explore", lib.ds_explore(space.h, C.byref(cfg) if cfg else None,
+                                       C.byref(io) if io else None, cb, None, cache.h,
+                                       C.byref(res), C.byref(tr) if tr else None))
+    del keep
+    return res, _trace_list(arr, tr)
+
+
+def ds_exploit(space, start, ecfg=None, cfg=None, io=None, cost=None, cache=None, trace_cap=0):
+    res = ds_tune_result()
+    arr, tr = _trace(trace_cap)
+    cb, keep = _callback(cost)
+    st = start if isinstance(start, ds_sched) else space.sched(start)
+    check("ds_exploit", lib.ds_exploit(space.h, C.byref(st), C.byref(ecfg) if ecfg else None,
+                                       C.byref(cfg) if cfg else None, C.byref(io) if io else None,
+                                       cb, None, cache.h if cache is not None else None,
+                                       C.byref(res), C.byref(tr) if tr else None))
+    del keep
+    return res, _trace_list(arr, tr)
+
+
+def ds_tune_tasks(spaces, weights, seeds, total_trials, cfg=None, ios=None, costs=None,
+                  rounds_cap=4096):
+    """One exploration budget over several tasks, then Droplet per task.
+    Returns (results[list of ds_tune_result], rounds[list of (task, n)], network_ms)."""
+    n = len(spaces)
+    tasks = (ds_task * n)()
+    keep = []
+    for t in range(n):
+        tasks[t].space = spaces[t].h
+        if ios is not None:
+            tasks[t].io = ios[t]
+        cb, k = _callback(costs[t] if costs is not None else None)
+        keep.append(k)
+        tasks[t].fn = cb
+        tasks[t].weight = float(weights[t])
+        tasks[t].seed = int(seeds[t])
+    results = (ds_tune_result * n)()
+    rounds = (ds_round * max(1, rounds_cap))()
+    nr, net = C.c_int(), C.c_double()
+    check("ds_tune_tasks", lib.ds_tune_tasks(tasks, n, int(total_trials),
+                                             C.byref(cfg) if cfg else None, results, rounds,
+                                             rounds_cap, C.byref(nr), C.byref(net)))
+    del keep
+    return (list(results), [(rounds[i].task, rounds[i].trials) for i in range(min(nr.value, rounds_cap))],
+            net.value)
 
 
 def droplet_tune(op, shape, start=None, budget=100):

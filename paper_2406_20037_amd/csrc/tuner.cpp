@@ -1,10 +1,14 @@
-// Exploration sampler, Droplet Search and the combined approach (Sections 2.1-2.3).
+// Exploration sampler, Droplet Search and the combined approach (Sections 2.1-2.3),
+// the exploitation strategies it is compared with (Section 3, RQ4) and the
+// whole-network trial split (Section 2.1, Termination in Ansor).
 #include <algorithm>
 #include <chrono>
 #include <cmath>
 #include <cstring>
 #include <functional>
 #include <limits>
+#include <memory>
+#include <new>
 #include <unordered_map>
 #include <unordered_set>
 
@@ -16,7 +20,21 @@ const Space &space_of(const ds_space *s);
 
 using namespace ds;
 
+// Measurements of one space, keyed by lattice key; remembers the space's axes
+// so that a cache cannot be used with another space.
+struct ds_cache {
+    int op = 0;
+    int64_t shape[9] = {0};
+    std::vector<std::vector<int32_t>> values;
+    std::unordered_map<uint64_t, Meas> map;
+};
+
 namespace {
+
+bool cache_fits(const ds_cache *c, const Space &sp) {
+    return c && c->op == sp.op && c->values == sp.values &&
+           std::equal(c->shape, c->shape + 9, sp.shape);
+}
 
 // SplitMix64 (Steele, Lea, Flood, OOPSLA 2014): state advances by the golden
 // gamma, output is the two-multiply finaliser of the state.
@@ -30,6 +48,8 @@ struct SplitMix64 {
         z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
         return z ^ (z >> 31);
     }
+    // Uniform double in [0, 1) from the top 53 bits.
+    double uniform01() { return double(next() >> 11) * (1.0 / 9007199254740992.0); }
     // Uniform on [0, n): reject the top partial block of 2^64 mod n values.
     uint32_t below(uint32_t n) {
         const uint64_t lim = (n & (n - 1)) == 0 ? 0 : (~uint64_t(0) / n) * n;
@@ -167,6 +187,196 @@ DropletOut droplet(const Space &sp, const int32_t *start, int budget, double alp
     out.best = cur;
     out.meas = cache[kcur];
     return out;
+}
+
+using Cache = std::unordered_map<uint64_t, Meas>;
+
+void note_best(double &best_so_far, const Meas &m) {
+    if (m.status == DS_OK) best_so_far = best_so_far > 0 ? std::min(best_so_far, m.median) : m.median;
+}
+
+struct ExploreOut {
+    int ib = -1;           // fastest drawn point (ties: first drawn)
+    double tb = std::numeric_limits<double>::infinity();
+    int measured = 0;
+    int failed = 0;
+};
+
+// Measures the drawn points into cache (cached points keep their measurement).
+ExploreOut explore(const Space &sp, const std::vector<std::vector<int32_t>> &pts, Cache &cache,
+                   const MeasureFn &measure, double &best_so_far, ds_trace *trace) {
+    ExploreOut out;
+    for (size_t i = 0; i < pts.size(); ++i) {
+        const uint64_t k = sp.key(pts[i].data());
+        auto it = cache.find(k);
+        if (it == cache.end()) {
+            Meas m = measure(pts[i].data(), best_so_far);
+            trace_push(trace, 0, m, k);
+            if (m.status != DS_OK) out.failed++;
+            note_best(best_so_far, m);
+            it = cache.emplace(k, std::move(m)).first;
+            out.measured++;
+        }
+        if (out.ib < 0 || it->second.median < out.tb) {
+            out.ib = int(i);
+            out.tb = it->second.median;
+        }
+    }
+    return out;
+}
+
+// Charging rules shared by Random, Grid and GA: cached candidates are skipped
+// without charge; an invalid candidate is a failed trial (or skipped when
+// valid_only); every other candidate is measured.
+struct ExploitRun {
+    const Space &sp;
+    Cache &cache;
+    const MeasureFn &measure;
+    int budget;
+    bool valid_only;
+    double &best_so_far;
+    ds_trace *trace;
+    int charged = 0;
+    int failed = 0;
+    std::vector<uint64_t> order;
+
+    bool exhausted() const { return charged >= budget; }
+
+    bool try_point(const int32_t *idx) {
+        const uint64_t k = sp.key(idx);
+        if (cache.count(k)) return false;
+        Meas m;
+        if (!sp.valid(idx)) {
+            if (valid_only) return false;
+            m.status = DS_EINVALID_SCHED;
+            m.median = std::numeric_limits<double>::infinity();
+            m.full.status = DS_EINVALID_SCHED;
+            m.full.median_ms = m.median;
+        } else {
+            m = measure(idx, best_so_far);
+            note_best(best_so_far, m);
+        }
+        if (m.status != DS_OK) failed++;
+        trace_push(trace, 2, m, k);
+        cache.emplace(k, std::move(m));
+        charged++;
+        order.push_back(k);
+        return true;
+    }
+};
+
+// Independent uniform draws of every axis index; ends after max_draws draws.
+struct RandomStream {
+    SplitMix64 &rng;
+    int64_t max_draws;
+    int64_t draws = 0;
+
+    bool next(const Space &sp, std::vector<int32_t> &out) {
+        if (draws >= max_draws) return false;
+        ++draws;
+        out.resize(sp.nknobs);
+        for (int a = 0; a < sp.nknobs; ++a) out[a] = int32_t(rng.below(uint32_t(sp.values[a].size())));
+        return true;
+    }
+};
+
+int roulette(SplitMix64 &rng, const std::vector<double> &w) {
+    double total = 0.0;
+    for (double v : w) total += v;
+    if (!(total > 0.0)) return int(rng.below(uint32_t(w.size())));
+    const double r = rng.uniform01() * total;
+    double cum = 0.0;
+    for (size_t i = 0; i < w.size(); ++i) {
+        cum += w[i];
+        if (cum > r) return int(i);
+    }
+    return int(w.size()) - 1;
+}
+
+double fitness(const Meas &m) {
+    if (m.status != DS_OK || !std::isfinite(m.median) || !(m.median > 0.0)) return 0.0;
+    return 1.0 / m.median;
+}
+
+// Genetic algorithm: generation zero is the start plus pop-1 Random draws; each
+// next generation keeps the `elite` fastest points seen so far and adds
+// children (roulette-selected parents, one-point crossover, per-gene mutation;
+// 50 attempts at a new point, then a Random draw).
+void run_ga(const Space &sp, ExploitRun &run, const std::vector<int32_t> &start, uint64_t seed,
+            int pop, int elite, double mutation) {
+    SplitMix64 rng(seed);
+    RandomStream rs{rng, 100 * int64_t(run.budget)};
+    const int d = sp.nknobs;
+    std::vector<uint64_t> seen{sp.key(start.data())};     // GA members in measurement order
+    std::vector<int32_t> tmp(d);
+    auto from_stream = [&](std::vector<int32_t> &out) {
+        while (rs.next(sp, tmp)) {
+            if (run.exhausted()) return false;
+            if (run.try_point(tmp.data())) {
+                seen.push_back(sp.key(tmp.data()));
+                out = tmp;
+                return true;
+            }
+        }
+        return false;
+    };
+    std::vector<std::vector<int32_t>> gen{start};
+    while (int(gen.size()) < pop && !run.exhausted()) {
+        std::vector<int32_t> p;
+        if (!from_stream(p)) break;
+        gen.push_back(p);
+    }
+    std::vector<int> rank;
+    std::vector<double> weights;
+    std::vector<int32_t> cand(d), p(d);
+    while (!run.exhausted() && !gen.empty()) {
+        rank.resize(seen.size());
+        for (size_t i = 0; i < seen.size(); ++i) rank[i] = int(i);
+        std::sort(rank.begin(), rank.end(), [&](int a, int b) {
+            const double ma = run.cache.at(seen[a]).median, mb = run.cache.at(seen[b]).median;
+            if (ma < mb) return true;
+            if (mb < ma) return false;
+            return a < b;
+        });
+        std::vector<std::vector<int32_t>> nxt;
+        for (int i = 0; i < elite && i < int(rank.size()); ++i) {
+            sp.from_key(seen[rank[i]], p.data());
+            nxt.push_back(p);
+        }
+        weights.resize(gen.size());
+        for (size_t i = 0; i < gen.size(); ++i)
+            weights[i] = fitness(run.cache.at(sp.key(gen[i].data())));
+        bool ended = false;
+        while (int(nxt.size()) < pop && !run.exhausted()) {
+            bool found = false;
+            for (int attempt = 0; attempt < 50; ++attempt) {
+                const int i = roulette(rng, weights);
+                const int j = roulette(rng, weights);
+                const int c = int(rng.below(uint32_t(d)));
+                for (int a = 0; a < d; ++a) cand[a] = a < c ? gen[i][a] : gen[j][a];
+                for (int a = 0; a < d; ++a)
+                    if (rng.uniform01() < mutation)
+                        cand[a] = int32_t(rng.below(uint32_t(sp.values[a].size())));
+                if (run.cache.count(sp.key(cand.data()))) continue;
+                if (run.valid_only && !sp.valid(cand.data())) continue;
+                found = true;
+                break;
+            }
+            if (found) {
+                run.try_point(cand.data());
+                seen.push_back(sp.key(cand.data()));
+                nxt.push_back(cand);
+            } else {
+                if (!from_stream(p)) {
+                    ended = true;
+                    break;
+                }
+                nxt.push_back(p);
+            }
+        }
+        gen.swap(nxt);
+        if (ended) break;
+    }
 }
 
 MeasureFn make_measure(const Space &sp, const ds_tune_cfg *cfg, const ds_tune_io *io,
@@ -413,36 +623,365 @@ int ds_tune(const ds_space *space, const ds_tune_cfg *cfg_in, const ds_tune_io *
         set_error("no valid point to sample");
         return DS_EEXHAUSTED;
     }
-    std::unordered_map<uint64_t, Meas> cache;
+    Cache cache;
     double best_so_far = 0.0;
-    int ib = -1, failed = 0;
-    double tb = std::numeric_limits<double>::infinity();
-    for (size_t i = 0; i < pts.size(); ++i) {
-        Meas m = measure(pts[i].data(), best_so_far);
-        const uint64_t k = sp.key(pts[i].data());
-        trace_push(trace, 0, m, k);
-        if (m.status != DS_OK) failed++;
-        else best_so_far = best_so_far > 0 ? std::min(best_so_far, m.median) : m.median;
-        if (ib < 0 || m.median < tb) {
-            ib = int(i);
-            tb = m.median;
-        }
-        cache[k] = m;
-    }
+    const ExploreOut e = explore(sp, pts, cache, measure, best_so_far, trace);
     const double t1 = now_s();
-    const DropletOut d = droplet(sp, pts[ib].data(), cfg.budget, cfg.alpha, cfg.frozen_mask,
+    const DropletOut d = droplet(sp, pts[e.ib].data(), cfg.budget, cfg.alpha, cfg.frozen_mask,
                                  cache, measure, best_so_far, trace);
     const double t2 = now_s();
     free_device(owned);
     fill_result(res, sp, d);
-    res->seed_point = make_sched(sp, pts[ib].data());
-    res->seed_ms = tb;
-    res->n_explore_measured = int(pts.size());
+    res->seed_point = make_sched(sp, pts[e.ib].data());
+    res->seed_ms = e.tb;
+    res->n_explore_measured = e.measured;
     res->n_droplet_measured = d.measured;
-    res->n_failed = failed + d.failed;
+    res->n_failed = e.failed + d.failed;
     res->explore_s = t1 - t0;
     res->droplet_s = t2 - t1;
     res->wall_s = t2 - t0;
+    return DS_OK;
+}
+
+int ds_cache_create(const ds_space *space, ds_cache **out) {
+    if (!space || !out) {
+        set_error("bad ds_cache_create arguments");
+        return DS_EINVAL;
+    }
+    const Space &sp = space_of(space);
+    ds_cache *c = new (std::nothrow) ds_cache;
+    if (!c) return DS_ENOMEM;
+    c->op = sp.op;
+    std::copy(sp.shape, sp.shape + 9, c->shape);
+    c->values = sp.values;
+    *out = c;
+    return DS_OK;
+}
+
+void ds_cache_destroy(ds_cache *cache) { delete cache; }
+
+int ds_cache_clone(const ds_cache *cache, ds_cache **out) {
+    if (!cache || !out) {
+        set_error("bad ds_cache_clone arguments");
+        return DS_EINVAL;
+    }
+    ds_cache *c = new (std::nothrow) ds_cache(*cache);
+    if (!c) return DS_ENOMEM;
+    *out = c;
+    return DS_OK;
+}
+
+int ds_cache_size(const ds_cache *cache) {
+    if (!cache) {
+        set_error("null cache");
+        return DS_EINVAL;
+    }
+    return int(cache->map.size());
+}
+
+int ds_cache_get(const ds_cache *cache, const ds_sched *s, ds_measurement *out) {
+    if (!cache || !s || !out || s->nknobs != int(cache->values.size())) {
+        set_error("bad ds_cache_get arguments");
+        return DS_EINVAL;
+    }
+    uint64_t key = 0, radix = 1;
+    for (size_t a = 0; a < cache->values.size(); ++a) {
+        const int n = int(cache->values[a].size());
+        if (s->idx[a] < 0 || s->idx[a] >= n) {
+            set_error("schedule index out of range");
+            return DS_EINVAL;
+        }
+        key += uint64_t(s->idx[a]) * radix;
+        radix *= uint64_t(n);
+    }
+    auto it = cache->map.find(key);
+    if (it == cache->map.end()) return 0;
+    *out = it->second.full;
+    out->status = it->second.status;
+    out->median_ms = it->second.median;
+    return 1;
+}
+
+int ds_explore(const ds_space *space, const ds_tune_cfg *cfg_in, const ds_tune_io *io,
+               ds_measure_fn fn, void *ctx, ds_cache *cache, ds_tune_result *res,
+               ds_trace *trace) {
+    if (!space || !res || !cache) {
+        set_error("bad ds_explore arguments");
+        return DS_EINVAL;
+    }
+    std::memset(res, 0, sizeof *res);
+    const Space &sp = space_of(space);
+    if (!cache_fits(cache, sp)) {
+        set_error("cache belongs to another space");
+        return DS_EINVAL;
+    }
+    ds_tune_cfg cfg;
+    if (cfg_in) cfg = *cfg_in;
+    else ds_tune_cfg_default(&cfg);
+    if (cfg.n_explore < 0) {
+        set_error("negative n_explore");
+        return DS_EINVAL;
+    }
+    if (trace) trace->n = 0;
+    float *owned = nullptr;
+    int rc = prepare(sp, &cfg, io, fn, &owned);
+    if (rc != DS_OK) return rc;
+    const MeasureFn measure = make_measure(sp, &cfg, io, owned ? owned : (io ? io->ref : nullptr),
+                                           fn, ctx);
+    const double t0 = now_s();
+    const auto pts = draw_points(sp, cfg.seed, cfg.n_explore);
+    if (pts.empty()) {
+        free_device(owned);
+        set_error("no valid point to sample");
+        return DS_EEXHAUSTED;
+    }
+    double best_so_far = 0.0;
+    const ExploreOut e = explore(sp, pts, cache->map, measure, best_so_far, trace);
+    free_device(owned);
+    const Meas &mb = cache->map.at(sp.key(pts[e.ib].data()));
+    res->seed_point = res->best = make_sched(sp, pts[e.ib].data());
+    res->seed_ms = res->best_ms = e.tb;
+    res->best_meas = mb.full;
+    res->n_explore_measured = e.measured;
+    res->n_failed = e.failed;
+    res->explore_s = res->wall_s = now_s() - t0;
+    return DS_OK;
+}
+
+void ds_exploit_cfg_default(ds_exploit_cfg *cfg) {
+    if (!cfg) return;
+    cfg->kind = DS_EXPLOIT_DROPLET;
+    cfg->budget = 100;
+    cfg->seed = 240620037ull;
+    cfg->valid_only = 0;
+    cfg->pop = 20;
+    cfg->elite = 3;
+    cfg->mutation = 0.1;
+}
+
+int ds_exploit(const ds_space *space, const ds_sched *start, const ds_exploit_cfg *cfg_in,
+               const ds_tune_cfg *tcfg_in, const ds_tune_io *io, ds_measure_fn fn, void *ctx,
+               ds_cache *cache, ds_tune_result *res, ds_trace *trace) {
+    if (!space || !start || !res) {
+        set_error("bad ds_exploit arguments");
+        return DS_EINVAL;
+    }
+    std::memset(res, 0, sizeof *res);
+    const Space &sp = space_of(space);
+    ds_exploit_cfg cfg;
+    if (cfg_in) cfg = *cfg_in;
+    else ds_exploit_cfg_default(&cfg);
+    ds_tune_cfg tcfg;
+    if (tcfg_in) tcfg = *tcfg_in;
+    else ds_tune_cfg_default(&tcfg);
+    if (cfg.kind < DS_EXPLOIT_DROPLET || cfg.kind > DS_EXPLOIT_GA || cfg.budget < 0 ||
+        (cfg.kind == DS_EXPLOIT_GA &&
+         (cfg.pop < 2 || cfg.elite < 0 || cfg.elite >= cfg.pop || !(cfg.mutation >= 0.0)))) {
+        set_error("bad exploitation settings");
+        return DS_EINVAL;
+    }
+    if (cache && !cache_fits(cache, sp)) {
+        set_error("cache belongs to another space");
+        return DS_EINVAL;
+    }
+    if (!sched_matches(sp, start) || !sp.in_range(start->idx)) {
+        set_error("start point does not belong to the space");
+        return DS_EINVAL;
+    }
+    if (!sp.valid(start->idx)) {
+        set_error("start point is not a valid schedule");
+        return DS_EINVALID_SCHED;
+    }
+    if (trace) trace->n = 0;
+    float *owned = nullptr;
+    int rc = prepare(sp, &tcfg, io, fn, &owned);
+    if (rc != DS_OK) return rc;
+    const MeasureFn measure = make_measure(sp, &tcfg, io, owned ? owned : (io ? io->ref : nullptr),
+                                           fn, ctx);
+    Cache local;
+    Cache &c = cache ? cache->map : local;
+    const std::vector<int32_t> st(start->idx, start->idx + sp.nknobs);
+    const uint64_t k0 = sp.key(st.data());
+    double best_so_far = 0.0;
+    for (const auto &kv : c) note_best(best_so_far, kv.second);
+    const double t0 = now_s();
+    if (cfg.kind == DS_EXPLOIT_DROPLET) {
+        const DropletOut d = droplet(sp, st.data(), cfg.budget, tcfg.alpha, tcfg.frozen_mask, c,
+                                     measure, best_so_far, trace);
+        fill_result(res, sp, d);
+        res->n_droplet_measured = d.measured;
+        res->n_failed = d.failed;
+    } else {
+        int start_measured = 0, start_failed = 0;
+        if (!c.count(k0)) {
+            Meas m = measure(st.data(), best_so_far);
+            trace_push(trace, 1, m, k0);
+            note_best(best_so_far, m);
+            start_failed = m.status != DS_OK;
+            c.emplace(k0, std::move(m));
+            start_measured = 1;
+        }
+        ExploitRun run{sp, c, measure, cfg.budget, cfg.valid_only != 0, best_so_far, trace};
+        if (cfg.kind == DS_EXPLOIT_RANDOM) {
+            SplitMix64 rng(cfg.seed);
+            RandomStream rs{rng, 100 * int64_t(cfg.budget)};
+            std::vector<int32_t> p;
+            while (!run.exhausted() && rs.next(sp, p)) run.try_point(p.data());
+        } else if (cfg.kind == DS_EXPLOIT_GRID) {
+            std::vector<int32_t> p(sp.nknobs);
+            for (uint64_t i = 1; i < sp.size && !run.exhausted(); ++i) {
+                sp.from_key((k0 + i) % sp.size, p.data());
+                run.try_point(p.data());
+            }
+        } else {
+            run_ga(sp, run, st, cfg.seed, cfg.pop, cfg.elite, cfg.mutation);
+        }
+        uint64_t kb = k0;
+        for (uint64_t k : run.order)
+            if (c.at(k).median < c.at(kb).median) kb = k;
+        std::vector<int32_t> b(sp.nknobs);
+        sp.from_key(kb, b.data());
+        res->best = make_sched(sp, b.data());
+        res->best_ms = c.at(kb).median;
+        res->best_meas = c.at(kb).full;
+        res->status = DS_OK;
+        res->n_droplet_measured = start_measured + run.charged;
+        res->n_failed = start_failed + run.failed;
+    }
+    free_device(owned);
+    res->seed_point = *start;
+    res->seed_ms = c.at(k0).median;
+    res->droplet_s = res->wall_s = now_s() - t0;
+    return DS_OK;
+}
+
+int ds_tune_tasks(const ds_task *tasks, int n_tasks, int total_trials, const ds_tune_cfg *cfg_in,
+                  ds_tune_result *results, ds_round *rounds, int rounds_cap, int *n_rounds,
+                  double *network_ms) {
+    if (!tasks || n_tasks <= 0 || total_trials < 0 || !results || (rounds_cap > 0 && !rounds) ||
+        rounds_cap < 0) {
+        set_error("bad ds_tune_tasks arguments");
+        return DS_EINVAL;
+    }
+    for (int t = 0; t < n_tasks; ++t)
+        if (!tasks[t].space || !(tasks[t].weight >= 0.0)) {
+            set_error("task %d has no space or a negative weight", t);
+            return DS_EINVAL;
+        }
+    ds_tune_cfg cfg;
+    if (cfg_in) cfg = *cfg_in;
+    else ds_tune_cfg_default(&cfg);
+    if (cfg.budget < 0) {
+        set_error("negative budget");
+        return DS_EINVAL;
+    }
+    const int q = std::max(1, std::min(total_trials / n_tasks, 64));
+    struct TaskState {
+        const Space *sp = nullptr;
+        float *owned = nullptr;
+        MeasureFn measure;
+        std::unique_ptr<SplitMix64> rng;
+        std::unordered_set<uint64_t> seen;
+        int64_t draws = 0;
+        int taken = 0;
+        bool ended = false;
+        Cache cache;
+        std::vector<int32_t> best;
+        double best_t = std::numeric_limits<double>::infinity();
+        double best_so_far = 0.0;
+        int failed = 0;
+        double explore_s = 0.0;
+    };
+    std::vector<TaskState> st(n_tasks);
+    int rc = DS_OK;
+    for (int t = 0; t < n_tasks && rc == DS_OK; ++t) {
+        TaskState &T = st[t];
+        T.sp = &space_of(tasks[t].space);
+        rc = prepare(*T.sp, &cfg, &tasks[t].io, tasks[t].fn, &T.owned);
+        if (rc != DS_OK) break;
+        T.measure = make_measure(*T.sp, &cfg, &tasks[t].io,
+                                 T.owned ? T.owned : tasks[t].io.ref, tasks[t].fn, tasks[t].ctx);
+        T.rng.reset(new SplitMix64(tasks[t].seed));
+    }
+    auto release = [&]() {
+        for (auto &T : st) free_device(T.owned);
+    };
+    if (rc != DS_OK) {
+        release();
+        return rc;
+    }
+    for (int t = 0; t < n_tasks; ++t) std::memset(&results[t], 0, sizeof results[t]);
+    int nr = 0;
+    int64_t spent = 0;
+    // Next n points of task t's sampler stream (the prefix rule of ansor_draw).
+    auto run_round = [&](int t, int n) {
+        TaskState &T = st[t];
+        const Space &sp = *T.sp;
+        const double t0 = now_s();
+        const int target = T.taken + n;
+        std::vector<int32_t> idx(sp.nknobs);
+        int got = 0;
+        while (T.taken < target && T.draws < 100 * int64_t(target)) {
+            ++T.draws;
+            for (int a = 0; a < sp.nknobs; ++a)
+                idx[a] = int32_t(T.rng->below(uint32_t(sp.values[a].size())));
+            const uint64_t k = sp.key(idx.data());
+            if (T.seen.count(k) || !sp.geometry(idx.data()).valid) continue;
+            T.seen.insert(k);
+            T.taken++;
+            got++;
+            Meas m = T.measure(idx.data(), T.best_so_far);
+            if (m.status != DS_OK) T.failed++;
+            note_best(T.best_so_far, m);
+            if (T.best.empty() || m.median < T.best_t) {
+                T.best = idx;
+                T.best_t = m.median;
+            }
+            T.cache.emplace(k, std::move(m));
+        }
+        if (T.taken < target) T.ended = true;
+        spent += got;
+        if (nr < rounds_cap) rounds[nr] = ds_round{t, got};
+        nr++;
+        T.explore_s += now_s() - t0;
+    };
+    for (int t = 0; t < n_tasks; ++t) run_round(t, q);
+    while (spent < total_trials) {
+        int pick = -1;
+        for (int t = 0; t < n_tasks; ++t) {
+            if (st[t].ended || st[t].best.empty()) continue;
+            if (pick < 0 || tasks[t].weight * st[t].best_t > tasks[pick].weight * st[pick].best_t)
+                pick = t;
+        }
+        if (pick < 0) break;
+        run_round(pick, int(std::min<int64_t>(q, total_trials - spent)));
+    }
+    double net = 0.0;
+    for (int t = 0; t < n_tasks; ++t) {
+        TaskState &T = st[t];
+        ds_tune_result &r = results[t];
+        r.n_explore_measured = T.taken;
+        r.explore_s = T.explore_s;
+        if (T.best.empty()) {
+            r.status = DS_EEXHAUSTED;
+            r.best_ms = r.seed_ms = std::numeric_limits<double>::infinity();
+            continue;
+        }
+        const double t0 = now_s();
+        const DropletOut d = droplet(*T.sp, T.best.data(), cfg.budget, cfg.alpha, cfg.frozen_mask,
+                                     T.cache, T.measure, T.best_so_far, nullptr);
+        fill_result(&r, *T.sp, d);
+        r.seed_point = make_sched(*T.sp, T.best.data());
+        r.seed_ms = T.best_t;
+        r.n_droplet_measured = d.measured;
+        r.n_failed = T.failed + d.failed;
+        r.droplet_s = now_s() - t0;
+        r.wall_s = r.explore_s + r.droplet_s;
+        net += tasks[t].weight * r.best_ms;
+    }
+    release();
+    if (n_rounds) *n_rounds = nr;
+    if (network_ms) *network_ms = net;
     return DS_OK;
 }
 
