@@ -287,12 +287,19 @@ def matmul_geometry(shape, v):
         uf = trip
     else:
         uf = min(trip, _pow2floor(max(1, v["unroll"] // body)))
-    stages = 2 if v["dbuf"] else 1
-    lds = stages * (bm * bk + bk * bn) * 4
+    # LDS stages: one without dbuf; with dbuf three when they fit, else two.
+    stage = bm * bk + bk * bn
+    stages = 1 if not v["dbuf"] else (3 if 3 * stage * 4 <= LDS_LIMIT else 2)
+    # A reduction split first splits every K-tile between two wave groups of
+    # one MFMA workgroup (when the K-tile has at least 8 steps); the rest of
+    # the split goes across workgroups.
+    kg = 2 if v["mfma"] and v["ks"] >= 2 and bk >= 8 else 1
+    wgs = v["ks"] // kg
+    lds = max(stages * stage, bm * bn if kg > 1 else 0) * 4
     nkt = _cdiv(K, bk)
-    grid = _cdiv(M, bm) * _cdiv(N, bn) * v["ks"]
-    threads = 256
-    valid = (ok and lds <= LDS_LIMIT and threads <= THREADS_LIMIT and v["ks"] <= nkt
+    grid = _cdiv(M, bm) * _cdiv(N, bn) * wgs
+    threads = 256 * kg
+    valid = (ok and lds <= LDS_LIMIT and threads <= THREADS_LIMIT and wgs <= nkt
              and grid <= GRID_LIMIT)
     return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=acc,
                 unroll_eff=uf, t0=t0, t1=t1, red=kstep, chunks=nkt)

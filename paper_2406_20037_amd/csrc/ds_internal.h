@@ -18,6 +18,16 @@ constexpr int kLdsLimit = 163840;     // bytes of LDS per workgroup on gfx950
 constexpr int kThreadsLimit = 1024;
 constexpr int64_t kGridLimit = 2147483647;
 
+// LDS stages of a matmul K-tile: one without dbuf; with dbuf three when they
+// fit in LDS (two tiles in flight while one is consumed), else two.
+constexpr int mm_stages(int bm, int bn, int bk, int dbuf) {
+    return !dbuf ? 1 : (int64_t(3) * (bm * bk + bk * bn) * 4 <= kLdsLimit ? 3 : 2);
+}
+
+// Wave groups splitting each K-tile of the MFMA matmul inside a workgroup:
+// two for a reduction split (ks >= 2) when the K-tile has at least 8 steps.
+constexpr int mm_wave_groups(int mfma, int ks, int bk) { return mfma && ks >= 2 && bk >= 8 ? 2 : 1; }
+
 struct Geometry {
     bool valid = false;
     int threads = 0;
@@ -127,7 +137,7 @@ int launch_plan(const Plan &plan, hipStream_t stream);
 const void *conv_valu_instance(int kpt, int ppt, int uf, int lds);
 const void *conv_mfma_instance(int tkb, int npb, int uf, int lds);
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf);
-const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf);
+const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf, int kg);
 int count_instances();
 
 // ---- measurement -----------------------------------------------------------------

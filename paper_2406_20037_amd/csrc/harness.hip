@@ -369,12 +369,13 @@ const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf) {
     return g_mm_valu[(((a * 5 + b) * 5 + k) * 7 + c) * 2 + dbuf];
 }
 
-const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf) {
+const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf, int kg) {
     const int a = log2_exact(wm) - 4, b = log2_exact(wn) - 4, k = log2_exact(bk) - 2,
               c = log2_exact(uf);
-    if (a < 0 || a > 3 || b < 0 || b > 3 || k < 0 || k > 4 || c < 0 || c > 6 || (dbuf & ~1))
+    if (a < 0 || a > 3 || b < 0 || b > 3 || k < 0 || k > 4 || c < 0 || c > 6 || (dbuf & ~1) ||
+        kg < 1 || kg > 2)
         return nullptr;
-    return g_mm_mfma[(((a * 4 + b) * 5 + k) * 7 + c) * 2 + dbuf];
+    return g_mm_mfma[((((a * 4 + b) * 5 + k) * 7 + c) * 2 + dbuf) * 2 + (kg - 1)];
 }
 
 int count_instances() {
@@ -450,7 +451,8 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         fill_mm_args(sp, x, w, y, a);
         const int bm = sp.value(s->idx, 0), bn = sp.value(s->idx, 1), bk = sp.value(s->idx, 2);
         const int dbuf = sp.value(s->idx, 4), mfma = sp.value(s->idx, 5);
-        a.ks = sp.value(s->idx, 6);
+        const int kg = mm_wave_groups(mfma, sp.value(s->idx, 6), bk);
+        a.ks = sp.value(s->idx, 6) / kg;
         a.tiles_m = int(cdiv64(a.M, bm));
         a.tiles_n = int(cdiv64(a.N, bn));
         a.nkt = int(g.chunks);
@@ -458,7 +460,7 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.vecA = (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
         a.vecB = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
         a.direct = a.vecA && a.vecB && a.M % bm == 0 && a.N % bn == 0 && a.K % bk == 0;
-        plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf)
+        plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf, kg)
                          : mm_valu_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf);
         plan.splits = a.ks > 1 ? int(cdiv64(a.nkt, a.kps)) : 1;
         plan.y_elems = int64_t(a.M) * a.N;

@@ -23,7 +23,7 @@ __device__ __forceinline__ int xcd_tile(int b, int nwg) {
 constexpr int kConvValuSlots = 7 * 5 * 5 * 2;   // KPT, PPT, UF, LDS
 constexpr int kConvMfmaSlots = 3 * 7 * 5 * 2;   // TKB, NPB, UF, LDS
 constexpr int kMmValuSlots = 5 * 5 * 5 * 7 * 2; // RM, RN, BK, UF, DB
-constexpr int kMmMfmaSlots = 4 * 4 * 5 * 7 * 2; // WM, WN, BK, UF, DB
+constexpr int kMmMfmaSlots = 4 * 4 * 5 * 7 * 2 * 2; // WM, WN, BK, UF, DB, KG
 
 constexpr int ilog2(int v) { return v <= 1 ? 0 : 1 + ilog2(v / 2); }
 constexpr int cmin(int a, int b) { return a < b ? a : b; }

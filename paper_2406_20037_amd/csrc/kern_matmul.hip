@@ -8,18 +8,21 @@
 //   Bs[BK][BN]  n contiguous.
 // When every tile is full and the operands are 16-byte aligned (a.direct), the
 // K-tiles travel straight from global memory into LDS (global_load_lds, no
-// register staging); with dbuf the next K-tile is in flight while the current
-// one is consumed.  Otherwise tiles are staged through registers with bounds
-// checks (zero outside A and B) and, with dbuf, written to the other LDS stage
-// after the current one is consumed.
+// register staging); with dbuf the next ST-1 K-tiles are in flight while the
+// current one is consumed (ST = 3 stages when they fit in LDS, else 2).
+// Otherwise tiles are staged through registers with bounds checks (zero
+// outside A and B) and, with dbuf, written to the other LDS stage after the
+// current one is consumed.
 //
 //   mm_valu: VALU FMA; thread (ty, tx) of a 16x16 grid owns RM rows x RN
 //            columns (contiguous).
-//   mm_mfma: 2x2 waves, each a WM x WN tile of fp32 MFMA blocks
-//            (v_mfma_f32_32x32x2f32 when WM, WN >= 32, else
-//            v_mfma_f32_16x16x4f32).  Lane group g feeds k = kk + VEC*g + v
-//            (v < VEC) to both operands, so one VEC-wide LDS read of A serves
-//            VEC MFMA steps.
+//   mm_mfma: KG groups of 2x2 waves; each wave a WM x WN tile of fp32 MFMA
+//            blocks (v_mfma_f32_32x32x2f32 when WM, WN >= 32, else
+//            v_mfma_f32_16x16x4f32).  Group g consumes the g-th of KG equal
+//            k ranges of every K-tile; the groups' accumulators are summed
+//            through LDS at the end (two waves per SIMD hide each other's
+//            waits).  Lane group g feeds k = kk + VEC*g + v (v < VEC) to both
+//            operands, so one VEC-wide LDS read of A serves VEC MFMA steps.
 // A split (ks > 1) stores its partial C tile; a reduce kernel sums the splits
 // into C in split order.
 #include <utility>
@@ -33,12 +36,21 @@ namespace {
 #define DS_GLOBAL(p) ((const __attribute__((address_space(1))) void *)(p))
 #define DS_LOCAL(p) ((__attribute__((address_space(3))) void *)(p))
 
+// Tiles in groups of up to kGroupM tile rows, column-major inside a group, so
+// the contiguous tile range of one XCD touches few rows of A and columns of B.
+constexpr int kGroupM = 4;
+
 __device__ __forceinline__ void mm_tile_coords(const MatmulArgs &a, int &mt, int &nt, int &z) {
-    int t = xcd_tile(blockIdx.x, gridDim.x);
-    nt = t % a.tiles_n;
-    t /= a.tiles_n;
-    mt = t % a.tiles_m;
-    z = t / a.tiles_m;
+    const int tiles = a.tiles_m * a.tiles_n;
+    const int t = xcd_tile(blockIdx.x, gridDim.x);
+    z = t / tiles;
+    const int r = t - z * tiles;
+    const int gsz = kGroupM * a.tiles_n;
+    const int g = r / gsz, first = g * kGroupM;
+    const int rows = min(a.tiles_m - first, kGroupM);
+    const int rg = r - g * gsz;
+    mt = first + rg % rows;
+    nt = rg / rows;
 }
 
 // Slot permutation of A row r (BK/4 slots per row).
@@ -58,8 +70,12 @@ __device__ __forceinline__ int a_off(int row, int k) {
 // Waits for every vector-memory operation of the wave, then for LDS, then
 // barriers the workgroup without a memory fence (the waits above make the LDS
 // writes of every wave complete before any wave passes).
+// s_waitcnt immediate for vmcnt(n) (expcnt, lgkmcnt not waited on).
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
+
+template <int VM = 0>
 __device__ __forceinline__ void stage_barrier() {
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(VM));
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
@@ -68,26 +84,26 @@ __device__ __forceinline__ void stage_barrier() {
 
 // Global -> LDS copy of one full, aligned K-tile (16 bytes per lane per
 // instruction; the LDS destination of a wave's instruction is contiguous).
-template <int BM, int BN, int BK>
+template <int BM, int BN, int BK, int NT>
 __device__ __forceinline__ void direct_load(const MatmulArgs &a, int m0, int n0, int kt, float *As,
                                             float *Bs) {
     constexpr int SPR = BK / 4, A4 = BM * SPR, B4 = BK * BN / 4;
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
 #pragma unroll
-    for (int j = 0; j < (A4 + 255) / 256; ++j) {
-        const int base = j * 256 + wid * 64;
+    for (int j = 0; j < (A4 + NT - 1) / NT; ++j) {
+        const int base = j * NT + wid * 64;
         const int c = base + lane;
-        if (A4 % 256 == 0 || c < A4) {
+        if (A4 % NT == 0 || c < A4) {
             const int row = c / SPR, slot = c % SPR;
             const float *src = a.A + (size_t)(m0 + row) * a.K + kt * BK + 4 * (slot ^ a_swz<BK>(row));
             __builtin_amdgcn_global_load_lds(DS_GLOBAL(src), DS_LOCAL(As + base * 4), 16, 0, 0);
         }
     }
 #pragma unroll
-    for (int j = 0; j < (B4 + 255) / 256; ++j) {
-        const int base = j * 256 + wid * 64;
+    for (int j = 0; j < (B4 + NT - 1) / NT; ++j) {
+        const int base = j * NT + wid * 64;
         const int c = base + lane;
-        if (B4 % 256 == 0 || c < B4) {
+        if (B4 % NT == 0 || c < B4) {
             const int k = c / (BN / 4), n4 = c % (BN / 4);
             const float *src = a.B + (size_t)(kt * BK + k) * a.N + n0 + 4 * n4;
             __builtin_amdgcn_global_load_lds(DS_GLOBAL(src), DS_LOCAL(Bs + base * 4), 16, 0, 0);
@@ -96,19 +112,19 @@ __device__ __forceinline__ void direct_load(const MatmulArgs &a, int m0, int n0,
 }
 
 // Global -> register staging of one K-tile (float4 slots; zero outside A, B).
-template <int BM, int BN, int BK>
+template <int BM, int BN, int BK, int NT>
 struct Stager {
     static constexpr int A4 = BM * BK / 4, B4 = BK * BN / 4;
-    static constexpr int AL = (A4 + 255) / 256, BL = (B4 + 255) / 256;
+    static constexpr int AL = (A4 + NT - 1) / NT, BL = (B4 + NT - 1) / NT;
     floatx4 ra[AL], rb[BL];
 
     __device__ __forceinline__ void load(const MatmulArgs &a, int m0, int n0, int kt) {
         const int tid = threadIdx.x;
 #pragma unroll
         for (int u = 0; u < AL; ++u) {
-            const int e = tid + 256 * u;
+            const int e = tid + NT * u;
             floatx4 v = {0.f, 0.f, 0.f, 0.f};
-            if (A4 % 256 == 0 || e < A4) {
+            if (A4 % NT == 0 || e < A4) {
                 const int m = e / (BK / 4), k4 = e - m * (BK / 4);
                 const int gm = m0 + m, gk = kt * BK + 4 * k4;
                 if (gm < a.M) {
@@ -126,9 +142,9 @@ struct Stager {
         }
 #pragma unroll
         for (int u = 0; u < BL; ++u) {
-            const int e = tid + 256 * u;
+            const int e = tid + NT * u;
             floatx4 v = {0.f, 0.f, 0.f, 0.f};
-            if (B4 % 256 == 0 || e < B4) {
+            if (B4 % NT == 0 || e < B4) {
                 const int k = e / (BN / 4), n4 = e - k * (BN / 4);
                 const int gk = kt * BK + k, gn = n0 + 4 * n4;
                 if (gk < a.K) {
@@ -150,16 +166,16 @@ struct Stager {
         const int tid = threadIdx.x;
 #pragma unroll
         for (int u = 0; u < AL; ++u) {
-            const int e = tid + 256 * u;
-            if (A4 % 256 == 0 || e < A4) {
+            const int e = tid + NT * u;
+            if (A4 % NT == 0 || e < A4) {
                 const int m = e / (BK / 4), k4 = e - m * (BK / 4);
                 *reinterpret_cast<floatx4 *>(As + a_off<BK>(m, 4 * k4)) = ra[u];
             }
         }
 #pragma unroll
         for (int u = 0; u < BL; ++u) {
-            const int e = tid + 256 * u;
-            if (B4 % 256 == 0 || e < B4) {
+            const int e = tid + NT * u;
+            if (B4 % NT == 0 || e < B4) {
                 const int k = e / (BN / 4), n4 = e - k * (BN / 4);
                 *reinterpret_cast<floatx4 *>(Bs + k * BN + 4 * n4) = rb[u];
             }
@@ -168,35 +184,50 @@ struct Stager {
 };
 
 // The K-loop shared by both families: stages K-tiles [kt0, kt1) through LDS
-// and calls compute(As, Bs) on each.
-template <int BM, int BN, int BK, int DB, class F>
+// and calls compute(As, Bs) on each.  NT threads; ST LDS stages (1: stage,
+// barrier, compute; >= 2: the next tiles are in flight during compute).
+template <int BM, int BN, int BK, int ST, int NT, class F>
 __device__ __forceinline__ void k_loop(const MatmulArgs &a, int m0, int n0, int kt0, int kt1,
                                        float *smem, F &&compute) {
     constexpr int STAGE = BM * BK + BK * BN;
     if (a.direct) {
-        if (DB) {
-            direct_load<BM, BN, BK>(a, m0, n0, kt0, smem, smem + BM * BK);
+        if constexpr (ST >= 2) {
+            // Each thread issues the same L copies per tile when the tile
+            // divides into whole rounds of NT threads; then waiting until at
+            // most L*(ST-2) copies are outstanding means tile kt has landed.
+            constexpr int A4 = BM * BK / 4, B4 = BK * BN / 4;
+            constexpr bool EXACT = A4 % NT == 0 && B4 % NT == 0;
+            constexpr int L = A4 / NT + B4 / NT;
+#pragma unroll
+            for (int p = 0; p < ST - 1; ++p)
+                if (kt0 + p < kt1)
+                    direct_load<BM, BN, BK, NT>(a, m0, n0, kt0 + p, smem + p * STAGE,
+                                                smem + p * STAGE + BM * BK);
+            int s = 0;
             for (int kt = kt0; kt < kt1; ++kt) {
-                const int s = (kt - kt0) & 1;
-                stage_barrier();
-                if (kt + 1 < kt1) {
-                    float *nx = smem + (s ^ 1) * STAGE;
-                    direct_load<BM, BN, BK>(a, m0, n0, kt + 1, nx, nx + BM * BK);
+                if (EXACT && ST > 2 && kt + ST - 2 < kt1) stage_barrier<EXACT ? L * (ST - 2) : 0>();
+                else stage_barrier<0>();
+                if (kt + ST - 1 < kt1) {
+                    int sn = s + ST - 1;
+                    if (sn >= ST) sn -= ST;
+                    float *nx = smem + sn * STAGE;
+                    direct_load<BM, BN, BK, NT>(a, m0, n0, kt + ST - 1, nx, nx + BM * BK);
                 }
                 compute(smem + s * STAGE, smem + s * STAGE + BM * BK);
+                if (++s == ST) s = 0;
             }
         } else {
             for (int kt = kt0; kt < kt1; ++kt) {
                 stage_barrier();
-                direct_load<BM, BN, BK>(a, m0, n0, kt, smem, smem + BM * BK);
+                direct_load<BM, BN, BK, NT>(a, m0, n0, kt, smem, smem + BM * BK);
                 stage_barrier();
                 compute(smem, smem + BM * BK);
             }
         }
         return;
     }
-    Stager<BM, BN, BK> st;
-    if (DB) {
+    Stager<BM, BN, BK, NT> st;
+    if constexpr (ST >= 2) {
         st.load(a, m0, n0, kt0);
         st.store(smem, smem + BM * BK);
         __syncthreads();
@@ -222,6 +253,7 @@ __device__ __forceinline__ void k_loop(const MatmulArgs &a, int m0, int n0, int 
 template <int RM, int RN, int BK, int UF, int DB>
 __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
     constexpr int BM = 16 * RM, BN = 16 * RN;
+    constexpr int ST = mm_stages(BM, BN, BK, DB);
     constexpr int U4 = UF >= 4 ? UF / 4 : 1;
     extern __shared__ float smem[];
     int mt, nt, z;
@@ -268,7 +300,7 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
             }
         }
     };
-    k_loop<BM, BN, BK, DB>(a, m0, n0, kt0, kt1, smem, compute);
+    k_loop<BM, BN, BK, ST, 256>(a, m0, n0, kt0, kt1, smem, compute);
 
     float *cbase = a.ks > 1 ? a.part + (size_t)z * a.M * a.N : a.C;
 #pragma unroll
@@ -284,17 +316,20 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
     }
 }
 
-template <int WM, int WN, int BK, int UF, int DB>
-__global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
+template <int WM, int WN, int BK, int UF, int DB, int KG>
+__global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
     constexpr int BM = 2 * WM, BN = 2 * WN;
+    constexpr int ST = mm_stages(BM, BN, BK, DB);
+    constexpr int KR = BK / KG;                // k of every K-tile per wave group
     constexpr bool BIG = WM >= 32 && WN >= 32;
     constexpr int IM = BIG ? 32 : 16;          // MFMA output tile edge
     constexpr int NG = 64 / IM;                // lane groups along k
-    constexpr int VEC = cmin(4, BK / NG);      // k values per lane per LDS read
-    constexpr int KG = NG * VEC;               // k consumed per group step
+    static_assert(KR >= NG, "every wave group needs one k step per lane group");
+    constexpr int VEC = cmin(4, KR / NG);      // k values per lane per LDS read
+    constexpr int KGS = NG * VEC;              // k consumed per group step
     constexpr int MB = WM / IM, NB = WN / IM;
     constexpr int KSTEP = BIG ? 2 : 4;
-    constexpr int UG = cmax(1, UF * KSTEP / KG);
+    constexpr int UG = cmax(1, UF * KSTEP / KGS);
     using Acc = typename std::conditional<BIG, floatx16, floatx4>::type;
 
     extern __shared__ float smem[];
@@ -304,7 +339,8 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
     if (kt0 >= kt1) return;
     const int m0 = mt * BM, n0 = nt * BN;
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wr = wid >> 1, wc = wid & 1;
+    const int kg = wid >> 2, wq = wid & 3;
+    const int wr = wq >> 1, wc = wq & 1;
     const int li = lane % IM, lg = lane / IM;
 
     Acc acc[MB][NB];
@@ -315,7 +351,7 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
 
     auto compute = [&](const float *As, const float *Bs) {
 #pragma unroll UG
-        for (int kk = 0; kk < BK; kk += KG) {
+        for (int kk = kg * KR; kk < (kg + 1) * KR; kk += KGS) {
             float av[MB][VEC];
 #pragma unroll
             for (int i = 0; i < MB; ++i) {
@@ -354,7 +390,30 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
             }
         }
     };
-    k_loop<BM, BN, BK, DB>(a, m0, n0, kt0, kt1, smem, compute);
+    k_loop<BM, BN, BK, ST, 256 * KG>(a, m0, n0, kt0, kt1, smem, compute);
+
+    constexpr int NV = BIG ? 16 : 4;
+    if constexpr (KG > 1) {
+        // group 1 hands its partial tile to group 0 through LDS
+        __syncthreads();
+        float *rb = smem + wq * (WM * WN);
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+#pragma unroll
+                    for (int v = 0; v < NV; ++v) rb[((i * NB + j) * NV + v) * 64 + lane] = acc[i][j][v];
+        }
+        __syncthreads();
+        if (kg == 1) return;
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+#pragma unroll
+                for (int v = 0; v < NV; ++v) acc[i][j][v] += rb[((i * NB + j) * NV + v) * 64 + lane];
+    }
 
     // Output layout: 32x32 block, lane holds rows 8*(v/4) + 4*lg + v%4 of
     // column li (v < 16); 16x16 block, rows 4*lg + v of column li (v < 4).
@@ -365,7 +424,6 @@ __global__ __launch_bounds__(256) void mm_mfma(MatmulArgs a) {
         for (int j = 0; j < NB; ++j) {
             const int gn = n0 + wc * WN + j * IM + li;
             if (gn >= a.N) continue;
-            constexpr int NV = BIG ? 16 : 4;
 #pragma unroll
             for (int v = 0; v < NV; ++v) {
                 const int row = BIG ? 8 * (v / 4) + 4 * lg + (v % 4) : 4 * lg + v;
@@ -397,41 +455,43 @@ void reg_mm_valu() {
     constexpr int DB = I % 2, iuf = (I / 2) % 7, ibk = (I / 14) % 5, irn = (I / 70) % 5,
                   irm = I / 350;
     constexpr int RM = 1 << irm, RN = 1 << irn, BK = kMmBkList[ibk], UF = 1 << iuf;
-    constexpr int lds = (DB ? 2 : 1) * (16 * RM * BK + BK * 16 * RN) * 4;
+    constexpr int lds = mm_stages(16 * RM, 16 * RN, BK, DB) * (16 * RM * BK + BK * 16 * RN) * 4;
     if constexpr (RM * RN <= 128 && UF <= BK && lds <= kLdsLimit &&
                   mm_uf_reachable(BK, RM * RN, UF) && I % DS_NSLICES == DS_SLICE)
         g_mm_valu[I] = reinterpret_cast<const void *>(&mm_valu<RM, RN, BK, UF, DB>);
 }
 
-// slot = (((iwm * 4 + iwn) * 5 + ibk) * 7 + log2 UF) * 2 + DB
+// slot = ((((iwm * 4 + iwn) * 5 + ibk) * 7 + log2 UF) * 2 + DB) * 2 + (KG - 1)
 template <int I>
 void reg_mm_mfma() {
-    constexpr int DB = I % 2, iuf = (I / 2) % 7, ibk = (I / 14) % 5, iwn = (I / 70) % 4,
-                  iwm = I / 280;
+    constexpr int KG = 1 + I % 2, DB = (I / 2) % 2, iuf = (I / 4) % 7, ibk = (I / 28) % 5,
+                  iwn = (I / 140) % 4, iwm = I / 560;
     constexpr int WM = kMmWaveList[iwm], WN = kMmWaveList[iwn], BK = kMmBkList[ibk],
                   UF = 1 << iuf;
     constexpr bool BIG = WM >= 32 && WN >= 32;
     constexpr int KSTEP = BIG ? 2 : 4;
     constexpr int blocks = BIG ? (WM / 32) * (WN / 32) : (WM / 16) * (WN / 16);
-    constexpr int lds = (DB ? 2 : 1) * (2 * WM * BK + BK * 2 * WN) * 4;
+    constexpr int lds = mm_stages(2 * WM, 2 * WN, BK, DB) * (2 * WM * BK + BK * 2 * WN) * 4;
     if constexpr (lds <= kLdsLimit && UF <= BK / KSTEP && mm_uf_reachable(BK / KSTEP, blocks, UF) &&
-                  I % DS_NSLICES == DS_SLICE)
-        g_mm_mfma[I] = reinterpret_cast<const void *>(&mm_mfma<WM, WN, BK, UF, DB>);
+                  (KG == 1 || BK >= 8) && I % DS_NSLICES == DS_SLICE)
+        g_mm_mfma[I] = reinterpret_cast<const void *>(&mm_mfma<WM, WN, BK, UF, DB, KG>);
 }
 
 template <size_t... I>
 void reg_all_valu(std::index_sequence<I...>) {
     (reg_mm_valu<int(I)>(), ...);
 }
-template <size_t... I>
+// in halves: one fold over every slot would exceed the compiler's nesting limit
+template <size_t Off, size_t... I>
 void reg_all_mfma(std::index_sequence<I...>) {
-    (reg_mm_mfma<int(I)>(), ...);
+    (reg_mm_mfma<int(Off + I)>(), ...);
 }
 
 struct Registrar {
     Registrar() {
         reg_all_valu(std::make_index_sequence<kMmValuSlots>{});
-        reg_all_mfma(std::make_index_sequence<kMmMfmaSlots>{});
+        reg_all_mfma<0>(std::make_index_sequence<kMmMfmaSlots / 2>{});
+        reg_all_mfma<kMmMfmaSlots / 2>(std::make_index_sequence<kMmMfmaSlots - kMmMfmaSlots / 2>{});
     }
 };
 const Registrar registrar;

@@ -166,13 +166,18 @@ Geometry mm_geometry(const int64_t *sh, const int32_t *v) {
         g.unroll_eff = trip;
     else
         g.unroll_eff = std::min(trip, pow2_floor(std::max(1, unroll / body)));
-    const int stages = dbuf ? 2 : 1;
-    g.lds_bytes = stages * (bm * bk + bk * bn) * 4;
+    // a reduction split first splits each K-tile between wave groups of one
+    // workgroup, then the K-tiles between workgroups (partials + reduce)
+    const int kg = mm_wave_groups(mfma, ks, bk);
+    const int wgs = ks / kg;
+    const int64_t lds = std::max<int64_t>(int64_t(mm_stages(bm, bn, bk, dbuf)) * (bm * bk + bk * bn),
+                                          kg > 1 ? int64_t(bm) * bn : 0) * 4;
+    g.lds_bytes = int(std::min<int64_t>(lds, INT32_MAX));
     g.red = kstep;
     g.chunks = cdiv(K, bk);
-    g.grid = cdiv(M, bm) * cdiv(N, bn) * ks;
-    g.threads = 256;
-    g.valid = ok && g.lds_bytes <= kLdsLimit && g.threads <= kThreadsLimit && ks <= g.chunks &&
+    g.grid = cdiv(M, bm) * cdiv(N, bn) * wgs;
+    g.threads = 256 * kg;
+    g.valid = ok && lds <= kLdsLimit && g.threads <= kThreadsLimit && wgs <= g.chunks &&
               g.grid <= kGridLimit;
     return g;
 }

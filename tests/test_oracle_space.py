@@ -113,12 +113,23 @@ def test_conv_geometry_hand_computed():
 def test_matmul_geometry_hand_computed():
     m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
     g = m.geometry(idx_of(m, bm=64, bn=64, bk=16, unroll=64, dbuf=1, mfma=1, ks=1))
-    assert g == dict(valid=True, grid=256, threads=256, lds_bytes=2 * (64 * 16 + 16 * 64) * 4,
+    # dbuf: three stages of 8 KiB fit.
+    assert g == dict(valid=True, grid=256, threads=256, lds_bytes=3 * (64 * 16 + 16 * 64) * 4,
                      acc=16, unroll_eff=8, t0=32, t1=32, red=2, chunks=64)
     g = m.geometry(idx_of(m, bm=32, bn=128, bk=32, unroll=16, dbuf=0, mfma=1, ks=4))
     # wave tile 16x64 -> 16x16x4 blocks: 1*4, acc 16; trip 8, 8*4 > 16 -> 16//4 = 4.
-    assert g == dict(valid=True, grid=32 * 8 * 4, threads=256, lds_bytes=(32 * 32 + 32 * 128) * 4,
+    # ks 4: two wave groups (512 threads) x two workgroup splits; LDS holds the
+    # larger of one stage (5120 floats) and the 32x128 partial tile (4096).
+    assert g == dict(valid=True, grid=32 * 8 * 2, threads=512, lds_bytes=(32 * 32 + 32 * 128) * 4,
                      acc=16, unroll_eff=4, t0=16, t1=64, red=4, chunks=32)
+    # dbuf with 2 x 64 KiB stages: three do not fit, two do.
+    g = m.geometry(idx_of(m, bm=128, bn=128, bk=64, unroll=0, dbuf=1, mfma=1, ks=1))
+    assert g["valid"] and g["lds_bytes"] == 2 * (128 * 64 + 64 * 128) * 4
+    # ks 2 with a K-tile of 4 steps stays a two-workgroup split of 256 threads.
+    g = m.geometry(idx_of(m, bm=64, bn=64, bk=4, unroll=0, dbuf=0, mfma=1, ks=2))
+    assert g["threads"] == 256 and g["grid"] == 16 * 16 * 2
+    # ks 2 with 256x256 tiles: the partial tile (256 KiB) does not fit in LDS.
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=8, unroll=0, dbuf=0, mfma=1, ks=2))
     g = m.geometry(idx_of(m, bm=128, bn=64, bk=8, unroll=512, dbuf=0, mfma=0, ks=1))
     assert g == dict(valid=True, grid=8 * 16, threads=256, lds_bytes=(128 * 8 + 8 * 64) * 4,
                      acc=32, unroll_eff=8, t0=8, t1=4, red=1, chunks=128)
