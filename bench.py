@@ -66,7 +66,7 @@ def describe(op, shape):
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="matmul_1024",
                     help="matmul_1024 | conv3x3_c64_56 | conv7x7_s2_c3_224 | resnet50 | vgg16")
@@ -288,7 +288,7 @@ def kernel_name(op, knobs, geom):
     if op == 2:
         if knobs["mfma"]:
             return (f"mm_mfma<{geom['t0']}, {geom['t1']}, {knobs['bk']}, {geom['unroll_eff']}, "
-                    f"{knobs['dbuf']}>")
+                    f"{knobs['dbuf']}, {geom['threads'] // 256}>")
         return (f"mm_valu<{geom['t0']}, {geom['t1']}, {knobs['bk']}, {geom['unroll_eff']}, "
                 f"{knobs['dbuf']}>")
     fam = "conv_mfma" if knobs["mfma"] else "conv_valu"
