@@ -38,6 +38,15 @@ def source_hash(kernel: str) -> str | None:
     return None
 
 
+def traffic_key(kernel: str, sched: str) -> str:
+    """Key of a kernel's HBM traffic entry: the instance and the schedule (the
+    same instance runs with different runtime tile arguments).  The unroll
+    knob is left out: it reaches the launch only through the instance's unroll
+    factor, which the instance name already carries."""
+    kept = [kv for kv in sched.split(",") if kv and not kv.startswith("unroll=")]
+    return f"{kernel} {','.join(kept)}" if kept else kernel
+
+
 def short(name: str) -> str:
     return (name.replace("ds::(anonymous namespace)::", "").replace("void ", "")
             .replace("(ds::MatmulArgs)", "").replace("(ds::ConvArgs)", ""))
@@ -71,6 +80,9 @@ def main(argv=None):
                     help="further --pmc runs: every counter per kernel (mean per dispatch)")
     ap.add_argument("--json-out", help="merge the scaled HBM bytes of our kernels into this file")
     ap.add_argument("--command", default="", help="recorded with the --json-out entries")
+    ap.add_argument("--sched", default="",
+                    help="schedule the profiled launches ran (knob=value,... in axis order); "
+                         "--json-out entries are keyed by kernel and schedule")
     args = ap.parse_args(argv)
     rows, n = top_kernels(args.trace, args.top)
     print(f"### Kernel trace ({n} distinct kernels; top {len(rows)} by total time)\n")
@@ -102,7 +114,7 @@ def main(argv=None):
             k = short(name)
             sh = source_hash(k)
             if sh:
-                entries[k] = {"fetch_kib": fv, "write_kib": wv, "read_factor": ff,
+                entries[traffic_key(k, args.sched)] = {"fetch_kib": fv, "write_kib": wv, "read_factor": ff,
                               "write_factor": wf, "read_bytes": fv * ff * 1024,
                               "write_bytes": wv * wf * 1024, "source_sha256": sh,
                               "command": args.command}
