@@ -52,24 +52,34 @@ __global__ void fill_kernel(float *p, int64_t n, float v) {
     if (tid < n - t0) p[t0 + tid] = v;
 }
 
-// y[i] = sum over z < splits of part[z * n + i], summed in split order.
+// y[i] = sum over z < S of part[z * n + i], summed in split order.  S is a
+// template parameter so every thread issues its S loads before the first add.
+template <int S>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float *__restrict__ part,
-                                                           float *__restrict__ y, int64_t n,
-                                                           int splits) {
+                                                           float *__restrict__ y, int64_t n) {
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
     const bool vec = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(y) % 16 == 0) &&
                      (reinterpret_cast<uintptr_t>(part) % 16 == 0);
     if (vec) {
         const int64_t n4 = n / 4;
+        const floatx4 *p4 = reinterpret_cast<const floatx4 *>(part);
         for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n4; i += stride) {
-            floatx4 s = reinterpret_cast<const floatx4 *>(part)[i];
-            for (int z = 1; z < splits; ++z) s += reinterpret_cast<const floatx4 *>(part + z * n)[i];
+            floatx4 v[S];
+#pragma unroll
+            for (int z = 0; z < S; ++z) v[z] = p4[z * n4 + i];
+            floatx4 s = v[0];
+#pragma unroll
+            for (int z = 1; z < S; ++z) s += v[z];
             reinterpret_cast<floatx4 *>(y)[i] = s;
         }
     } else {
         for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-            float s = part[i];
-            for (int z = 1; z < splits; ++z) s += part[z * n + i];
+            float v[S];
+#pragma unroll
+            for (int z = 0; z < S; ++z) v[z] = part[z * n + i];
+            float s = v[0];
+#pragma unroll
+            for (int z = 1; z < S; ++z) s += v[z];
             y[i] = s;
         }
     }
@@ -494,6 +504,10 @@ int fill_async(float *p, int64_t n, float v, hipStream_t stream) {
 
 int launch_plan(const Plan &plan, hipStream_t stream) {
     if (plan.grid == 0 || plan.y_elems == 0) return DS_OK;
+    if (plan.splits > 8) {      // the lattice's split axis stops at 8
+        set_error("more than 8 reduction splits");
+        return DS_EUNSUPPORTED;
+    }
     int rc = ensure_lds_attr(plan.func, plan.lds);
     if (rc != DS_OK) return rc;
     void *args[1];
@@ -508,8 +522,20 @@ int launch_plan(const Plan &plan, hipStream_t stream) {
         const float *part = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.part : plan.mm.part;
         const int64_t n4 = cdiv64(plan.y_elems, 4);
         const int64_t blocks = std::min<int64_t>(cdiv64(n4, 256), 4096);
-        hipLaunchKernelGGL(split_reduce_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, part, y,
-                           plan.y_elems, plan.splits);
+        const void *reduce[] = {nullptr, nullptr,
+                                reinterpret_cast<const void *>(&split_reduce_kernel<2>),
+                                reinterpret_cast<const void *>(&split_reduce_kernel<3>),
+                                reinterpret_cast<const void *>(&split_reduce_kernel<4>),
+                                reinterpret_cast<const void *>(&split_reduce_kernel<5>),
+                                reinterpret_cast<const void *>(&split_reduce_kernel<6>),
+                                reinterpret_cast<const void *>(&split_reduce_kernel<7>),
+                                reinterpret_cast<const void *>(&split_reduce_kernel<8>)};
+        int64_t n = plan.y_elems;
+        void *rargs[] = {const_cast<float **>(&part), &y, &n};
+        if (!hip_ok(hipLaunchKernel(reduce[plan.splits], dim3(unsigned(blocks)), dim3(256), rargs, 0,
+                                    stream),
+                    "split reduce launch"))
+            return DS_EHIP;
         if (!hip_ok(hipGetLastError(), "split reduce launch")) return DS_EHIP;
     }
     return DS_OK;

@@ -33,6 +33,14 @@ __device__ __forceinline__ int fdiv(int n, FastDiv f) {
     return int((__umulhi(unsigned(n), f.m) + unsigned(n)) >> f.s);
 }
 
+// A zero in device memory: loads of positions that read zero are pointed here.
+__device__ const float kZero[1] = {0.f};
+
+// Global-memory pointers (a select between two generic pointers would make
+// the load a flat load, whose wait counts are conservative).
+typedef const __attribute__((address_space(1))) float gfloat;
+__device__ __forceinline__ gfloat *gptr(const float *p) { return (gfloat *)(p); }
+
 __device__ __forceinline__ void conv_tile_coords(const ConvArgs &a, int &n, int &z, int &kt,
                                                  int &pt, int &qt) {
     int t = xcd_tile(blockIdx.x, gridDim.x);
@@ -95,14 +103,14 @@ __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, in
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int e = e0 + u * nt;
-            v[u] = 0.f;
-            if (e < nh) {
-                const int c_l = fdiv(e, a.f_hw), rem = e - c_l * hw;
-                const int hy = fdiv(rem, a.f_ws), hx = rem - hy * a.ws;
-                const int c = c0 + c_l, gy = hy0 + hy, gx = hx0 + hx;
-                if (c < a.C && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W)
-                    v[u] = xn[((size_t)c * a.H + gy) * a.W + gx];
-            }
+            // unconditional load (element 0 where the position reads zero),
+            // select after: a guarded load would drain the loads in flight
+            const int c_l = fdiv(e, a.f_hw), rem = e - c_l * hw;
+            const int hy = fdiv(rem, a.f_ws), hx = rem - hy * a.ws;
+            const int c = c0 + c_l, gy = hy0 + hy, gx = hx0 + hx;
+            const bool ok = e < nh && c < a.C && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+            const float t = xn[ok ? ((size_t)c * a.H + gy) * a.W + gx : 0];
+            v[u] = ok ? t : 0.f;
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
@@ -118,14 +126,12 @@ __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, in
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int e = e0 + u * nt;
-            v[u] = 0.f;
-            if (e < nw) {
-                const int kl = fdiv(e, a.f_red), kr = e - kl * a.red;
-                const int k = kt * a.tk + kl;
-                int gofs;
-                if (weight_src(a, kr, c0, real, crs, gofs) && k < a.K)
-                    v[u] = a.w[(size_t)k * crs + gofs];
-            }
+            const int kl = fdiv(e, a.f_red), kr = e - kl * a.red;
+            const int k = kt * a.tk + kl;
+            int gofs;
+            const bool ok = e < nw && weight_src(a, kr, c0, real, crs, gofs) && k < a.K;
+            const float t = a.w[ok ? (size_t)k * crs + gofs : 0];
+            v[u] = ok ? t : 0.f;
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
@@ -281,12 +287,15 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
                 for (int j = 0; j < PPT; ++j) {
                     const int iy = iy0[j] + r, ix = ix0[j] + s;
                     const bool ok = cok && pv[j] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
-                    xv[j] = ok ? xc[goff + iy0[j] * a.W + ix0[j]] : 0.f;
+                    const float t = xc[ok ? goff + iy0[j] * a.W + ix0[j] : 0];
+                    xv[j] = ok ? t : 0.f;
                 }
 #pragma unroll
                 for (int i = 0; i < KPT; ++i) {
                     const int k = k0 + i;
-                    const float wv = (cok && k < a.K) ? a.w[(size_t)k * crs + c0 * RS + kr] : 0.f;
+                    const bool wok = cok && k < a.K;
+                    const float t = a.w[wok ? (size_t)k * crs + c0 * RS + kr : 0];
+                    const float wv = wok ? t : 0.f;
 #pragma unroll
                     for (int j = 0; j < PPT; ++j) acc[i][j] = fmaf(wv, xv[j], acc[i][j]);
                 }
@@ -397,8 +406,11 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         } else {
             if (ci == ci0) __syncthreads();
             const float *xc = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
-#pragma unroll UG
-            for (int kg = 0; kg < ngroups; ++kg) {
+            // Software pipeline: the operands of the next 16-step group are
+            // loaded while the MFMAs of the current one run.  Positions that
+            // read zero load the zero in device memory, so no select waits on
+            // a load.
+            auto gload = [&](int kg, float (&A)[4][TKB], float (&B)[4][NPB]) {
                 const int kb = kg * 16 + 4 * lg;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -408,25 +420,39 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
                     const int c_l = int((info >> 16) & 0x7fffu);
                     const int r = int((info >> 8) & 0xffu), s = int(info & 0xffu);
                     const bool cok = (info & 0x80000000u) && c0 + c_l < a.C;
-                    float av[TKB];
 #pragma unroll
                     for (int i = 0; i < TKB; ++i) {
                         const int k = kt * a.tk + i * 16 + li;
-                        av[i] = (cok && k < a.K) ? a.w[(size_t)k * crs + c0 * RS + kr] : 0.f;
+                        const bool wok = cok && k < a.K;
+                        A[v][i] = *(wok ? gptr(a.w + (size_t)k * crs + c0 * RS + kr) : gptr(kZero));
                     }
-                    float bv[NPB];
 #pragma unroll
                     for (int b = 0; b < NPB; ++b) {
                         const int iy = iy0[b] + r, ix = ix0[b] + s;
                         const bool ok = cok && pv[b] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
-                        bv[b] = ok ? xc[goff + iy0[b] * a.W + ix0[b]] : 0.f;
+                        B[v][b] = *(ok ? gptr(xc + goff + iy0[b] * a.W + ix0[b]) : gptr(kZero));
                     }
+                }
+            };
+            auto gmma = [&](const float (&A)[4][TKB], const float (&B)[4][NPB]) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
 #pragma unroll
                     for (int i = 0; i < TKB; ++i)
 #pragma unroll
                         for (int b = 0; b < NPB; ++b)
-                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[b],
+                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[v][i], B[v][b],
                                                                             acc[i][b], 0, 0, 0);
+            };
+            float A0[4][TKB], B0[4][NPB], A1[4][TKB], B1[4][NPB];
+            gload(0, A0, B0);
+            for (int kg = 0; kg < ngroups; kg += 2) {
+                const bool two = kg + 1 < ngroups;
+                if (two) gload(kg + 1, A1, B1);
+                gmma(A0, B0);
+                if (two) {
+                    if (kg + 2 < ngroups) gload(kg + 2, A0, B0);
+                    gmma(A1, B1);
                 }
             }
         }
