@@ -226,12 +226,14 @@ def conv_geometry(shape, v):
         wrow = red
         t0, t1 = kpt, ppt           # template parameters: channels and pixels per thread
     else:
-        # Four waves split the pixels; each wave covers all tk channels in
-        # 16x16 blocks (v_mfma_f32_16x16x4f32).
-        threads = 256
-        ok = tk >= 16 and npx >= 64
+        # Up to four waves split the pixels (one per 16-pixel block for tiles
+        # under 64 pixels); each wave covers all tk channels in 16x16 blocks
+        # (v_mfma_f32_16x16x4f32).
+        waves = min(4, max(1, npx // 16))
+        threads = 64 * waves
+        ok = tk >= 16 and npx >= 16
         tkb = max(1, tk // 16)
-        npb = max(1, npx // 64)
+        npb = max(1, npx // (16 * waves))
         acc = 4 * tkb * npb
         body = tkb * npb
         ok = ok and acc <= 128

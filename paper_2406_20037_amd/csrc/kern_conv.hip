@@ -10,8 +10,9 @@
 //   conv_valu: VALU FMA.  Lanes take pixels first, then groups of KPT output
 //              channels; each lane accumulates KPT x PPT outputs.
 //   conv_mfma: implicit GEMM on v_mfma_f32_16x16x4f32 (M = channels, N =
-//              pixels, K = kr).  Four waves split the pixels of the tile; a
-//              wave holds TKB x NPB 16x16 blocks.  Lane group g (lanes
+//              pixels, K = kr).  Up to four waves split the pixels of the tile
+//              (one per 16-pixel block below 64 pixels); a wave holds TKB x
+//              NPB 16x16 blocks.  Lane group g (lanes
 //              16g..16g+15) feeds reduction steps kr = 16*j + 4*g + v, v < 4,
 //              for both operands, so a 16-byte LDS read gives four steps of A.
 //              Operands of the next 16-step group are read while the MFMAs of

@@ -95,10 +95,12 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         g.t0 = kpt;
         g.t1 = ppt;
     } else {
-        // Four waves split the pixels; 16x16 output blocks per wave.
-        g.threads = 256;
-        ok = tk >= 16 && npx >= 64;
-        const int tkb = std::max(1, tk / 16), npb = std::max(1, npx / 64);
+        // Up to four waves split the pixels (one per 16-pixel block for tiles
+        // under 64 pixels); 16x16 output blocks per wave.
+        const int waves = std::min(4, std::max(1, npx / 16));
+        g.threads = 64 * waves;
+        ok = tk >= 16 && npx >= 16;
+        const int tkb = std::max(1, tk / 16), npb = std::max(1, npx / (16 * waves));
         g.acc = 4 * tkb * npb;
         body = tkb * npb;
         ok = ok && g.acc <= 128;

@@ -109,6 +109,7 @@ PARITY_CASES = [
     ("matmul_ragged", 2, (129, 67, 300), 250),
     ("matmul_fc", 2, (1, 1000, 2048), 120),
     ("matmul_k_odd", 2, (33, 45, 7), 150),
+    ("conv_7x7_out", 1, (2, 32, 7, 7, 48, 3, 3, 1, 1), 200),
 ]
 
 
@@ -134,6 +135,7 @@ EXACT_CASES = [
     ("conv7x7_s2", 1, (1, 3, 60, 60, 16, 7, 7, 2, 3)),
     ("matmul_ragged", 2, (129, 67, 300)),
     ("matmul_256", 2, (256, 256, 512)),
+    ("conv_7x7_out", 1, (2, 32, 7, 7, 48, 3, 3, 1, 1)),
 ]
 
 

@@ -99,15 +99,36 @@ def test_conv_geometry_hand_computed():
     assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2100 + 48)
     # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
     assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
-    # MFMA needs >= 16 channels and >= 64 pixels.
+    # MFMA needs >= 16 channels and >= 16 pixels (one 16x16 block per wave).
     assert not s.valid(idx_of(s, tk=8, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
-    assert not s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
+    assert not s.valid(idx_of(s, tk=16, th=2, tw=4, tc=4, unroll=0, lds=0, ks=1, mfma=1))
+    assert s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
     # LDS limit: 64-channel chunk of a 34x34 halo does not fit (one chunk, one
     # buffer of 16*576 + 64*34*34 + 1 -> 83204 floats).
     g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0))
     assert g["lds_bytes"] == 4 * (83204 + 576) and not g["valid"]
     # split finer than the chunk count.
     assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0))
+
+
+def test_conv_mfma_small_tile_geometry():
+    # 7x7 outputs: a 4x4 tile (16 pixels) runs on one wave.  Reduction chunk
+    # 16 channels x 9 taps = 144 (a multiple of 16), weight row 148; halo 6x6;
+    # 32 chunks over 8 splits -> two LDS buffers of
+    # ceil((16*148 + 16*36 + 1) / 4) * 4 = 2948 floats, then the 144-entry table.
+    s = sp.Space(sp.OP_CONV, (1, 512, 7, 7, 512, 3, 3, 1, 1))
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=4, tc=16, unroll=64, lds=1, ks=8, mfma=1))
+    assert g == dict(valid=True, grid=8 * 32 * 2 * 2, threads=64, lds_bytes=4 * (2 * 2948 + 144),
+                     acc=4, unroll_eff=16, t0=1, t1=1, red=144, chunks=32)
+    # two 16-channel blocks on the one wave
+    g = s.geometry(idx_of(s, tk=32, th=4, tw=4, tc=16, unroll=0, lds=0, ks=4, mfma=1))
+    assert g["valid"] and g["threads"] == 64 and g["t0"] == 2 and g["t1"] == 1
+    # 8 pixels: less than one 16-pixel block
+    assert not s.valid(idx_of(s, tk=32, th=4, tw=2, tc=16, unroll=0, lds=0, ks=4, mfma=1))
+    # 32 pixels: two waves, one block each.
+    c = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
+    g = c.geometry(idx_of(c, tk=16, th=4, tw=8, tc=16, unroll=0, lds=1, ks=1, mfma=1))
+    assert g["valid"] and g["threads"] == 128 and g["t1"] == 1
 
 
 def test_matmul_geometry_hand_computed():
