@@ -391,17 +391,24 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
                                 acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(
                                     av[i][v], bv[v][b], acc[i][b], 0, 0, 0);
                 };
+                // The loop body has no branch: the wait counts stay exact, so
+                // the MFMAs of one group never wait for the next group's reads.
                 floatx4 a0[TKB], a1[TKB];
                 float b0[4][NPB], b1[4][NPB];
                 load(0, a0, b0);
-                for (int kg = 0; kg < ngroups; kg += 2) {
-                    const bool two = kg + 1 < ngroups;
-                    if (two) load(kg + 1, a1, b1);
+                int kg = 0;
+                for (; kg + 2 < ngroups; kg += 2) {
+                    load(kg + 1, a1, b1);
                     mma(a0, b0);
-                    if (two) {
-                        if (kg + 2 < ngroups) load(kg + 2, a0, b0);
-                        mma(a1, b1);
-                    }
+                    load(kg + 2, a0, b0);
+                    mma(a1, b1);
+                }
+                if (kg + 1 < ngroups) {
+                    load(kg + 1, a1, b1);
+                    mma(a0, b0);
+                    mma(a1, b1);
+                } else {
+                    mma(a0, b0);
                 }
             }
         } else {
@@ -447,14 +454,19 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
             };
             float A0[4][TKB], B0[4][NPB], A1[4][TKB], B1[4][NPB];
             gload(0, A0, B0);
-            for (int kg = 0; kg < ngroups; kg += 2) {
-                const bool two = kg + 1 < ngroups;
-                if (two) gload(kg + 1, A1, B1);
+            int kg = 0;
+            for (; kg + 2 < ngroups; kg += 2) {
+                gload(kg + 1, A1, B1);
                 gmma(A0, B0);
-                if (two) {
-                    if (kg + 2 < ngroups) gload(kg + 2, A0, B0);
-                    gmma(A1, B1);
-                }
+                gload(kg + 2, A0, B0);
+                gmma(A1, B1);
+            }
+            if (kg + 1 < ngroups) {
+                gload(kg + 1, A1, B1);
+                gmma(A0, B0);
+                gmma(A1, B1);
+            } else {
+                gmma(A0, B0);
             }
         }
     }
