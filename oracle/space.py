@@ -247,7 +247,8 @@ def conv_geometry(shape, v):
         # weights + halo (+ one zero float) per buffer, rounded to 16 bytes; two
         # buffers when a workgroup walks more than one chunk; then the table.
         nbuf = 2 if _cdiv(chunks, v["ks"]) > 1 else 1
-        lds = 4 * (nbuf * _cdiv(tk * wrow + tc * hs * ws + 1, 4) * 4 + red)
+        # + the reduction table and one source offset per staged position
+        lds = 4 * (nbuf * _cdiv(tk * wrow + tc * hs * ws + 1, 4) * 4 + red + tk * wrow + tc * hs * ws)
     else:
         lds = 8 * red
     grid = N * v["ks"] * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)

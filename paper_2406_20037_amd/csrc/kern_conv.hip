@@ -18,7 +18,8 @@
 //              Operands of the next 16-step group are read while the MFMAs of
 //              the current one run.
 //
-// LDS layout (lds=1): [weights tk x wrow][input halo tc x hs x ws][zero][table red]
+// LDS layout (lds=1): [weights tk x wrow][input halo tc x hs x ws][zero] per buffer,
+//                    then [table red][weight sources tk x wrow][halo sources tc x hs x ws]
 //             (lds=0): [table red x {offset, info}]
 // A split (ks > 1) stores its partial output tile; a reduce kernel sums the
 // splits into y in split order.
@@ -204,12 +205,80 @@ __device__ __forceinline__ void chunk_barrier() {
 }
 
 // Stages chunk ci of this workgroup into LDS buffer b.
+// Source offsets of every LDS position of one chunk, relative to the chunk's
+// base (weights: row kt*tk, column c0*R*S; halo: image n, channel c0), -1
+// where the position reads zero.  Identical for every chunk that ends at or
+// before channel C, so they are built once per workgroup.
+__device__ __forceinline__ void build_stage_tables(const ConvArgs &a, int kt, int pt, int qt,
+                                                   int *wsrc, int *xsrc) {
+    const int RS = a.R * a.S;
+    const int real = a.tc * RS;
+    const int crs = a.C * RS;
+    const int npw = a.tk * a.wrow;
+    for (int p = threadIdx.x; p < npw; p += blockDim.x) {
+        const int kl = fdiv(p, a.f_wrow), kr = p - kl * a.wrow;
+        wsrc[p] = kr < real && kt * a.tk + kl < a.K ? kl * crs + kr : -1;
+    }
+    const int hw = a.hs * a.ws;
+    const int nh = a.tc * hw;
+    const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
+    for (int p = threadIdx.x; p < nh; p += blockDim.x) {
+        const int c_l = fdiv(p, a.f_hw), rem = p - c_l * hw;
+        const int hy = fdiv(rem, a.f_ws), hx = rem - hy * a.ws;
+        const int gy = hy0 + hy, gx = hx0 + hx;
+        xsrc[p] = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W ? (c_l * a.H + gy) * a.W + gx : -1;
+    }
+}
+
+// dma_chunk driven by the tables: one table read and one copy per position;
+// positions that read zero are never written (both buffers are zeroed once).
+__device__ __forceinline__ void dma_chunk_tab(const ConvArgs &a, int n, int kt, int c0,
+                                              const int *wsrc, const int *xsrc, float *wt,
+                                              float *xs) {
+    const int RS = a.R * a.S;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nwv = blockDim.x >> 6;
+    const float *wb = a.w + (size_t)kt * a.tk * a.C * RS + (size_t)c0 * RS;
+    const float *xb = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
+    const int npw = a.tk * a.wrow;
+    for (int base = wid * 64; base < npw; base += nwv * 64) {
+        const int p = base + lane;
+        const int e = p < npw ? wsrc[p] : -1;
+        if (e >= 0)
+            __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + e), DS_LOCAL(wt + base), 4, 0, 0);
+    }
+    const int nh = a.tc * a.hs * a.ws;
+    for (int base = wid * 64; base < nh; base += nwv * 64) {
+        const int p = base + lane;
+        const int e = p < nh ? xsrc[p] : -1;
+        if (e >= 0)
+            __builtin_amdgcn_global_load_lds(DS_GLOBAL(xb + e), DS_LOCAL(xs + base), 4, 0, 0);
+    }
+}
+
+// LDS staging set-up of a workgroup: the offset tables and zeroed buffers for
+// the table-driven copies (whole waves only), then a barrier.
+__device__ __forceinline__ void stage_init(const ConvArgs &a, float *smem, int kt, int pt, int qt,
+                                           int *wsrc, int *xsrc) {
+    if ((blockDim.x & 63) == 0) {
+        build_stage_tables(a, kt, pt, qt, wsrc, xsrc);
+        floatx4 *z4 = reinterpret_cast<floatx4 *>(smem);
+        for (int e = threadIdx.x; e < (a.nbuf * a.buf) >> 2; e += blockDim.x)
+            z4[e] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    __syncthreads();
+}
+
 __device__ __forceinline__ void stage_to(const ConvArgs &a, float *smem, int b, int n, int kt, int pt,
-                                         int qt, int ci) {
+                                         int qt, int ci, const int *wsrc, const int *xsrc) {
     float *wt = smem + b * a.buf;
     float *xs = wt + a.tk * a.wrow;
-    if ((blockDim.x & 63) == 0) dma_chunk(a, n, kt, pt, qt, ci * a.tc, wt, xs);
-    else stage_chunk(a, n, kt, pt, qt, ci * a.tc, wt, xs);
+    const int c0 = ci * a.tc;
+    if ((blockDim.x & 63) == 0) {
+        if (c0 + a.tc <= a.C) dma_chunk_tab(a, n, kt, c0, wsrc, xsrc, wt, xs);
+        else dma_chunk(a, n, kt, pt, qt, c0, wt, xs);      // channel tail
+    } else {
+        stage_chunk(a, n, kt, pt, qt, c0, wt, xs);
+    }
 }
 
 template <int KPT, int PPT, int UF, int LDS>
@@ -246,8 +315,12 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         for (int j = 0; j < PPT; ++j) acc[i][j] = 0.f;
 
     int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
+    int *wsrc = tab + a.red, *xsrc = wsrc + a.tk * a.wrow;     // LDS staging tables
     build_table(a, tab, LDS);
-    if (LDS) stage_to(a, smem, 0, n, kt, pt, qt, ci0);
+    if (LDS) {
+        stage_init(a, smem, kt, pt, qt, wsrc, xsrc);
+        stage_to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
+    }
 
     const int RS = a.R * a.S;
     const int crs = a.C * RS;
@@ -256,7 +329,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         if (LDS) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
-            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1);
+            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             const float *wg = wt + g * KPT * a.wrow;
@@ -349,8 +422,12 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         for (int b = 0; b < NPB; ++b) acc[i][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
+    int *wsrc = tab + a.red, *xsrc = wsrc + a.tk * a.wrow;     // LDS staging tables
     build_table(a, tab, LDS);
-    if (LDS) stage_to(a, smem, 0, n, kt, pt, qt, ci0);
+    if (LDS) {
+        stage_init(a, smem, kt, pt, qt, wsrc, xsrc);
+        stage_to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
+    }
 
     constexpr int UG = UF >= 4 ? UF / 4 : 1;   // 16-step groups unrolled
     const int RS = a.R * a.S;
@@ -361,7 +438,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         if (LDS) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
-            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1);
+            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             {

@@ -117,7 +117,8 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         // workgroup walks more than one chunk, then the offset table.
         const int64_t nbuf = cdiv(g.chunks, ks) > 1 ? 2 : 1;
         const int64_t buf = cdiv(int64_t(tk) * wrow + tc * hs * ws + 1, 4) * 4;
-        lds_bytes = 4 * (nbuf * buf + int64_t(g.red));
+        // + the reduction table and the staging source tables
+        lds_bytes = 4 * (nbuf * buf + int64_t(g.red) + int64_t(tk) * wrow + int64_t(tc) * hs * ws);
     } else {
         lds_bytes = 8 * int64_t(g.red);
     }

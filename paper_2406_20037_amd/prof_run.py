@@ -19,7 +19,8 @@ sys.path.insert(0, ROOT)
 
 def main(argv=None):
     ap = argparse.ArgumentParser()
-    ap.add_argument("--workload", default="matmul_1024")
+    ap.add_argument("--workload", default="matmul_1024",
+                    help="a single-kernel workload or a network layer (resnet50:NAME, vgg16:NAME)")
     ap.add_argument("--sched", required=True, help="knob=value,... (every axis)")
     ap.add_argument("--iters", type=int, default=100)
     ap.add_argument("--copy-mib", type=int, default=64)
@@ -31,16 +32,23 @@ def main(argv=None):
     from synthdata import workloads as wl
     from paper_2406_20037_amd import _lib as L
 
-    op, shape = wl.SINGLE[args.workload]
+    if ":" in args.workload:          # a network layer, e.g. vgg16:L6_256_256_56
+        net, layer = args.workload.split(":", 1)
+        table = {"resnet50": wl.RESNET50, "vgg16": wl.VGG16}[net]
+        op, shape = next((o, sh) for name, o, sh, _ in table if name == layer)
+        kind = "he"
+    else:
+        op, shape = wl.SINGLE[args.workload]
+        kind = "uniform"
     knobs = {k: int(v) for k, v in (kv.split("=") for kv in args.sched.split(","))}
     space = L.Space(op, shape)
     s = space.sched_of(**knobs)
     if op == wl.OP_CONV:
-        x, w = synthdata.conv_inputs(shape, "uniform")
+        x, w = synthdata.conv_inputs(shape, kind)
         N, C, H, W, K, R, S, st, pd = shape
         n_out = N * K * ((H + 2 * pd - R) // st + 1) * ((W + 2 * pd - S) // st + 1)
     else:
-        x, w = synthdata.matmul_inputs(shape, "uniform")
+        x, w = synthdata.matmul_inputs(shape, kind)
         n_out = shape[0] * shape[1]
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     yd = torch.empty(n_out, device="cuda:0")

@@ -79,24 +79,26 @@ def test_conv_geometry_hand_computed():
     # 64 pixels -> one 16-pixel block per wave; 16 channels -> one block.
     # reduction 16*9 = 144; halo 10x10; LDS 4*(16*100+1) + 4*16*144 + 4*144.
     # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148; 4 chunks
-    # in one split -> two buffers of 16*148 + 16*100 + 1 -> 3972 floats, + table.
-    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256, lds_bytes=4 * (2 * 3972 + 144), acc=4,
+    # in one split -> two buffers of 16*148 + 16*100 + 1 -> 3972 floats, + table,
+    # + one staging source per weight and halo position (2368 + 1600).
+    assert g == dict(valid=True, grid=4 * 7 * 7, threads=256,
+                     lds_bytes=4 * (2 * 3972 + 144 + 2368 + 1600), acc=4,
                      unroll_eff=16, t0=1, t1=1, red=144, chunks=4)
     g = s.geometry(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0))
     # 128 pixels x 4 channels -> 256 threads, 2 channel groups of 2; unroll 16//2 = 8.
     assert g == dict(valid=True, grid=2 * 16 * 14 * 2, threads=256, lds_bytes=8 * 72, acc=2,
                      unroll_eff=8, t0=2, t1=1, red=72, chunks=8)
     # One pixel, 64 channels: one wave, one channel per lane; 32 chunks -> two
-    # buffers of 64*18 + 2*3*3 + 1 = 1171 -> 1172 floats, + table.
+    # buffers of 64*18 + 2*3*3 + 1 = 1171 -> 1172 floats, + table, + sources.
     g = s.geometry(idx_of(s, tk=64, th=1, tw=1, tc=2, unroll=0, lds=1, ks=1, mfma=0))
-    assert g == dict(valid=True, grid=56 * 56, threads=64, lds_bytes=4 * (2 * 1172 + 18),
+    assert g == dict(valid=True, grid=56 * 56, threads=64, lds_bytes=4 * (2 * 1172 + 18 + 1152 + 18),
                      acc=1, unroll_eff=1, t0=1, t1=1, red=18, chunks=32)
     # Fewer than 64 outputs: not a full wave.
     assert not s.valid(idx_of(s, tk=2, th=4, tw=4, tc=1, unroll=0, lds=0, ks=1, mfma=0))
     # MFMA reduction padded to a multiple of 16: 4 channels x 9 taps = 36 -> 48;
     # 16 chunks -> two buffers of 32*52 + 4*6*18 + 1 = 2097 -> 2100 floats.
     g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1))
-    assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2100 + 48)
+    assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2100 + 48 + 1664 + 432)
     # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
     assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
     # MFMA needs >= 16 channels and >= 16 pixels (one 16x16 block per wave).
@@ -106,7 +108,7 @@ def test_conv_geometry_hand_computed():
     # LDS limit: 64-channel chunk of a 34x34 halo does not fit (one chunk, one
     # buffer of 16*576 + 64*34*34 + 1 -> 83204 floats).
     g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0))
-    assert g["lds_bytes"] == 4 * (83204 + 576) and not g["valid"]
+    assert g["lds_bytes"] == 4 * (83204 + 576 + 9216 + 73984) and not g["valid"]
     # split finer than the chunk count.
     assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0))
 
@@ -115,10 +117,12 @@ def test_conv_mfma_small_tile_geometry():
     # 7x7 outputs: a 4x4 tile (16 pixels) runs on one wave.  Reduction chunk
     # 16 channels x 9 taps = 144 (a multiple of 16), weight row 148; halo 6x6;
     # 32 chunks over 8 splits -> two LDS buffers of
-    # ceil((16*148 + 16*36 + 1) / 4) * 4 = 2948 floats, then the 144-entry table.
+    # ceil((16*148 + 16*36 + 1) / 4) * 4 = 2948 floats, then the 144-entry table
+    # and the staging sources (2368 + 576).
     s = sp.Space(sp.OP_CONV, (1, 512, 7, 7, 512, 3, 3, 1, 1))
     g = s.geometry(idx_of(s, tk=16, th=4, tw=4, tc=16, unroll=64, lds=1, ks=8, mfma=1))
-    assert g == dict(valid=True, grid=8 * 32 * 2 * 2, threads=64, lds_bytes=4 * (2 * 2948 + 144),
+    assert g == dict(valid=True, grid=8 * 32 * 2 * 2, threads=64,
+                     lds_bytes=4 * (2 * 2948 + 144 + 2368 + 576),
                      acc=4, unroll_eff=16, t0=1, t1=1, red=144, chunks=32)
     # two 16-channel blocks on the one wave
     g = s.geometry(idx_of(s, tk=32, th=4, tw=4, tc=16, unroll=0, lds=0, ks=4, mfma=1))
