@@ -450,6 +450,8 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.f_rs = make_fastdiv(a.R * a.S);
         a.f_s = make_fastdiv(a.S);
         a.f_wrow = make_fastdiv(a.wrow);
+        a.w4 = (a.C * a.R * a.S) % 4 == 0 && (a.tc * a.R * a.S) % 4 == 0 && a.wrow % 4 == 0 &&
+               reinterpret_cast<uintptr_t>(w) % 16 == 0;
         a.nbuf = cdiv64(a.chunks, a.ks) > 1 ? 2 : 1;
         a.buf = int(cdiv64(int64_t(a.tk) * a.wrow + int64_t(a.tc) * a.hs * a.ws + 1, 4) * 4);
         plan.func = mfma ? conv_mfma_instance(g.t0, g.t1, g.unroll_eff, lds)

@@ -215,9 +215,18 @@ __device__ __forceinline__ void build_stage_tables(const ConvArgs &a, int kt, in
     const int real = a.tc * RS;
     const int crs = a.C * RS;
     const int npw = a.tk * a.wrow;
-    for (int p = threadIdx.x; p < npw; p += blockDim.x) {
-        const int kl = fdiv(p, a.f_wrow), kr = p - kl * a.wrow;
-        wsrc[p] = kr < real && kt * a.tk + kl < a.K ? kl * crs + kr : -1;
+    if (a.w4) {
+        // 16-byte groups: a group of four positions is valid or not as a whole
+        for (int q = threadIdx.x; q < (npw >> 2); q += blockDim.x) {
+            const int p = q << 2;
+            const int kl = fdiv(p, a.f_wrow), kr = p - kl * a.wrow;
+            wsrc[q] = kr < real && kt * a.tk + kl < a.K ? kl * crs + kr : -1;
+        }
+    } else {
+        for (int p = threadIdx.x; p < npw; p += blockDim.x) {
+            const int kl = fdiv(p, a.f_wrow), kr = p - kl * a.wrow;
+            wsrc[p] = kr < real && kt * a.tk + kl < a.K ? kl * crs + kr : -1;
+        }
     }
     const int hw = a.hs * a.ws;
     const int nh = a.tc * hw;
@@ -240,11 +249,23 @@ __device__ __forceinline__ void dma_chunk_tab(const ConvArgs &a, int n, int kt, 
     const float *wb = a.w + (size_t)kt * a.tk * a.C * RS + (size_t)c0 * RS;
     const float *xb = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
     const int npw = a.tk * a.wrow;
-    for (int base = wid * 64; base < npw; base += nwv * 64) {
-        const int p = base + lane;
-        const int e = p < npw ? wsrc[p] : -1;
-        if (e >= 0)
-            __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + e), DS_LOCAL(wt + base), 4, 0, 0);
+    if (a.w4) {
+        // 16 bytes per lane: one instruction fills 256 consecutive floats
+        const int ng = npw >> 2;
+        for (int base = wid * 64; base < ng; base += nwv * 64) {
+            const int q = base + lane;
+            const int e = q < ng ? wsrc[q] : -1;
+            if (e >= 0)
+                __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + e), DS_LOCAL(wt + 4 * base), 16, 0,
+                                                 0);
+        }
+    } else {
+        for (int base = wid * 64; base < npw; base += nwv * 64) {
+            const int p = base + lane;
+            const int e = p < npw ? wsrc[p] : -1;
+            if (e >= 0)
+                __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + e), DS_LOCAL(wt + base), 4, 0, 0);
+        }
     }
     const int nh = a.tc * a.hs * a.ws;
     for (int base = wid * 64; base < nh; base += nwv * 64) {
