@@ -60,6 +60,7 @@ __device__ __forceinline__ void conv_tile_coords(const ConvArgs &a, int &n, int 
 // entries real..red-1 are padding: their weights are zero, and in LDS mode they
 // point at the first halo element (a finite value inside the halo for every
 // pixel offset); in global mode their valid bit is clear and they read zero.
+// LDS mode stores byte offsets, so a read address is one add to a lane base.
 __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool lds) {
     const int RS = a.R * a.S;
     const int real = a.tc * RS;
@@ -67,7 +68,7 @@ __device__ __forceinline__ void build_table(const ConvArgs &a, int *tab, bool ld
         const int c_l = fdiv(e, a.f_rs), rs = e - c_l * RS;
         const int r = fdiv(rs, a.f_s), s = rs - r * a.S;
         if (lds) {
-            tab[e] = e < real ? c_l * a.hs * a.ws + r * a.ws + s : 0;
+            tab[e] = 4 * (e < real ? c_l * a.hs * a.ws + r * a.ws + s : 0);   // bytes
         } else {
             tab[2 * e] = e < real ? c_l * a.H * a.W + r * a.W + s : 0;
             tab[2 * e + 1] = e < real ? int(0x80000000u | unsigned(c_l << 16) | unsigned(r << 8) |
@@ -354,12 +355,15 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             const float *wg = wt + g * KPT * a.wrow;
+            const char *xp[PPT];
+#pragma unroll
+            for (int j = 0; j < PPT; ++j) xp[j] = reinterpret_cast<const char *>(xs + poff[j]);
 #pragma unroll UF
             for (int kr = 0; kr < a.red; ++kr) {
                 const int off = tab[kr];
                 float xv[PPT];
 #pragma unroll
-                for (int j = 0; j < PPT; ++j) xv[j] = xs[off + poff[j]];
+                for (int j = 0; j < PPT; ++j) xv[j] = *reinterpret_cast<const float *>(xp[j] + off);
 #pragma unroll
                 for (int i = 0; i < KPT; ++i) {
                     const float wv = wg[i * a.wrow + kr];
@@ -463,21 +467,28 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             {
+                // lane bases: pixel b of the halo, row i*16+li of the weights
+                const char *bp[NPB];
+#pragma unroll
+                for (int b = 0; b < NPB; ++b) bp[b] = reinterpret_cast<const char *>(xs + poff[b]);
+                const float *ap[TKB];
+#pragma unroll
+                for (int i = 0; i < TKB; ++i) ap[i] = wt + (i * 16 + li) * a.wrow + 4 * lg;
                 // Two groups per iteration with two named operand sets: the
                 // reads of group kg+1 are issued before the MFMAs of group kg
                 // (LDS returns in order, so those MFMAs need not wait for them).
                 auto load = [&](int kg, floatx4 (&av)[TKB], float (&bv)[4][NPB]) {
                     const int kb = kg * 16 + 4 * lg;
-                    int off[4];
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) off[v] = tab[kb + v];
+                    const int4 off = *reinterpret_cast<const int4 *>(tab + kb);
+                    const int offv[4] = {off.x, off.y, off.z, off.w};
 #pragma unroll
                     for (int i = 0; i < TKB; ++i)
-                        av[i] = *reinterpret_cast<const floatx4 *>(wt + (i * 16 + li) * a.wrow + kb);
+                        av[i] = *reinterpret_cast<const floatx4 *>(ap[i] + kg * 16);
 #pragma unroll
                     for (int v = 0; v < 4; ++v)
 #pragma unroll
-                        for (int b = 0; b < NPB; ++b) bv[v][b] = xs[off[v] + poff[b]];
+                        for (int b = 0; b < NPB; ++b)
+                            bv[v][b] = *reinterpret_cast<const float *>(bp[b] + offv[v]);
                 };
                 auto mma = [&](const floatx4 (&av)[TKB], const float (&bv)[4][NPB]) {
 #pragma unroll
