@@ -316,6 +316,191 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
     }
 }
 
+// Geometry of one wave group's MFMA work on a K-tile.
+template <int WM, int WN, int BK, int KG>
+struct MfmaShape {
+    static constexpr bool BIG = WM >= 32 && WN >= 32;
+    static constexpr int IM = BIG ? 32 : 16;          // MFMA output tile edge
+    static constexpr int NG = 64 / IM;                // lane groups along k
+    static constexpr int KR = BK / KG;                // k of every K-tile per wave group
+    static constexpr int VEC = cmin(4, KR / NG);      // k values per lane per LDS read
+    static constexpr int KGS = NG * VEC;              // k consumed per chunk
+    static constexpr int NCH = KR / KGS;              // chunks per K-tile
+    static constexpr int MB = WM / IM, NB = WN / IM;
+    static constexpr int NV = BIG ? 16 : 4;           // accumulator values per lane
+};
+
+// Whether the direct path runs software-pipelined (mm_mfma_pipe): at least
+// two stages, every thread issuing the same number of copies per K-tile, and
+// at least two chunks per K-tile.
+template <int WM, int WN, int BK, int DB, int KG>
+constexpr bool mm_pipelined() {
+    using S = MfmaShape<WM, WN, BK, KG>;
+    constexpr int BM = 2 * WM, BN = 2 * WN, NT = 256 * KG;
+    return mm_stages(BM, BN, BK, DB) >= 2 && (BM * BK / 4) % NT == 0 && (BK * BN / 4) % NT == 0 &&
+           S::NCH >= 2;
+}
+
+// Direct (global -> LDS) K-loop with the LDS operand reads software-pipelined
+// across MFMA chunks.  A chunk is one k step of every MFMA block of the wave
+// (KGS k values).  The operands of chunk c + D are read while the MFMAs of
+// chunk c run, from a ring of D + 1 operand sets (D = 3 with unroll >= 16 when
+// the chunks of a K-tile divide into whole rings, else 1).  The stage barrier
+// sits before the last D chunks of every K-tile: past it every wave has
+// finished reading the current tile and the next tile has landed, so the next
+// tile's first reads overlap the current tile's last MFMAs, and the stage of
+// the tile just consumed is refilled in the next iteration.  Each K-tile's
+// copies are spread over the chunks before the barrier.  Past the end of the
+// split the last K-tile is loaded again into a stage nobody reads, so every
+// iteration has the same copies in flight and the wait counts are constants.
+template <int WM, int WN, int BK, int UF, int DB, int KG, class Acc, int MB, int NB>
+__device__ __forceinline__ void mm_mfma_pipe(const MatmulArgs &a, int m0, int n0, int kt0, int kt1,
+                                             float *smem, Acc (&acc)[MB][NB]) {
+    using S = MfmaShape<WM, WN, BK, KG>;
+    constexpr int BM = 2 * WM, BN = 2 * WN, NT = 256 * KG;
+    constexpr int ST = mm_stages(BM, BN, BK, DB);
+    constexpr int STAGE = BM * BK + BK * BN;
+    constexpr int SPR = BK / 4, A4 = BM * SPR, B4 = BK * BN / 4;
+    constexpr int AL = A4 / NT, BL = B4 / NT, L = AL + BL;
+    constexpr int IM = S::IM, VEC = S::VEC, KGS = S::KGS, NCH = S::NCH;
+    constexpr int D = UF >= 16 && NCH % 4 == 0 ? 3 : 1;
+    constexpr int RG = D + 1;
+    constexpr bool RING = NCH % RG == 0;   // chunk c always uses ring slot c % RG
+    constexpr int PRE = NCH - D;           // chunks before the stage barrier
+    constexpr int PER = (L + PRE - 1) / PRE;
+    static_assert(PRE >= 1, "the copies of a tile are issued before its barrier");
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wsc = __builtin_amdgcn_readfirstlane(wid);
+    const int kg = wid >> 2, wq = wid & 3;
+    const int wr = wq >> 1, wc = wq & 1;
+    const int li = lane % IM, lg = lane / IM;
+
+    // per-thread sources of K-tile 0; a tile adds kt*BK (A) or kt*BK*N (B)
+    const float *pa[AL], *pb[BL];
+#pragma unroll
+    for (int j = 0; j < AL; ++j) {
+        const int c = j * NT + wid * 64 + lane;
+        const int row = c / SPR, slot = c % SPR;
+        pa[j] = a.A + (size_t)(m0 + row) * a.K + 4 * (slot ^ a_swz<BK>(row));
+    }
+#pragma unroll
+    for (int j = 0; j < BL; ++j) {
+        const int c = j * NT + wid * 64 + lane;
+        const int k = c / (BN / 4), n4 = c % (BN / 4);
+        pb[j] = a.B + (size_t)k * a.N + n0 + 4 * n4;
+    }
+    // copy j of K-tile kt into the stage at st (the LDS slot is wave-uniform)
+    auto copy = [&](int kt, float *st, int j) {
+        if (j < AL) {
+            __builtin_amdgcn_global_load_lds(DS_GLOBAL(pa[j] + (size_t)kt * BK),
+                                             DS_LOCAL(st + (j * NT + wsc * 64) * 4), 16, 0, 0);
+        } else {
+            const int jb = j - AL;
+            __builtin_amdgcn_global_load_lds(DS_GLOBAL(pb[jb] + (size_t)kt * BK * a.N),
+                                             DS_LOCAL(st + BM * BK + (jb * NT + wsc * 64) * 4), 16,
+                                             0, 0);
+        }
+    };
+
+    struct Ops {
+        float a[MB][VEC];
+        float b[VEC][NB];
+    };
+    const int arow = wr * WM + li;
+    const int bcol = BM * BK + wc * WN + li;
+    auto read = [&](const float *st, int c, Ops &o) {
+        const int k = kg * S::KR + c * KGS + VEC * lg;
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            const float *src = st + a_off<BK>(arow + i * IM, k);
+            if constexpr (VEC == 4) {
+                const floatx4 t = *reinterpret_cast<const floatx4 *>(src);
+                o.a[i][0] = t[0];
+                o.a[i][1] = t[1];
+                o.a[i][2] = t[2];
+                o.a[i][3] = t[3];
+            } else if constexpr (VEC == 2) {
+                const float2 t = *reinterpret_cast<const float2 *>(src);
+                o.a[i][0] = t.x;
+                o.a[i][1] = t.y;
+            } else {
+                o.a[i][0] = src[0];
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) o.b[v][j] = st[bcol + (k + v) * BN + j * IM];
+    };
+    auto mma = [&](const Ops &o) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    if constexpr (S::BIG)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(o.a[i][v], o.b[v][j],
+                                                                        acc[i][j], 0, 0, 0);
+                    else
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[i][v], o.b[v][j],
+                                                                        acc[i][j], 0, 0, 0);
+                }
+    };
+    // one LDS read between consecutive MFMAs of a chunk
+    auto interleave = [&]() {
+        constexpr int NM = VEC * MB * NB, NDS = MB + (VEC * NB + 1) / 2;
+#pragma unroll
+        for (int t = 0; t < NM; ++t) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (t < NDS && t + 1 < NM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+    };
+
+    // prologue: K-tiles kt0 .. kt0+ST-2, then wait for the first
+#pragma unroll
+    for (int p = 0; p < ST - 1; ++p)
+#pragma unroll
+        for (int j = 0; j < L; ++j) copy(min(kt0 + p, kt1 - 1), smem + p * STAGE, j);
+    stage_barrier<L * (ST - 2)>();
+    Ops o[RG];
+#pragma unroll
+    for (int c = 0; c < D; ++c) read(smem, c, o[c]);
+
+    int s = 0;
+    for (int kt = kt0; kt < kt1; ++kt) {
+        int sp = s + ST - 1;
+        if (sp >= ST) sp -= ST;
+        int sn = s + 1;
+        if (sn == ST) sn = 0;
+        const float *cur = smem + s * STAGE, *nxt = smem + sn * STAGE;
+        float *fill = smem + sp * STAGE;
+        const int ktf = min(kt + ST - 1, kt1 - 1);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            if (c == PRE) stage_barrier<L * (ST - 2)>();
+            Ops &rd = RING ? o[(c + D) % RG] : o[D];
+            if (c + D < NCH) read(cur, c + D, rd);
+            else read(nxt, c + D - NCH, rd);
+            mma(RING ? o[c % RG] : o[0]);
+            if (c < PRE) {
+#pragma unroll
+                for (int q = 0; q < PER; ++q)
+                    if (c * PER + q < L) copy(ktf, fill, c * PER + q);
+            }
+            interleave();
+            if constexpr (!RING) {
+#pragma unroll
+                for (int r = 0; r < D; ++r) o[r] = o[r + 1];
+            }
+        }
+        s = sn;
+    }
+    // the reloads past the end are still in flight
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+}
+
 template <int WM, int WN, int BK, int UF, int DB, int KG>
 __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
     constexpr int BM = 2 * WM, BN = 2 * WN;
@@ -390,7 +575,12 @@ __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
             }
         }
     };
-    k_loop<BM, BN, BK, ST, 256 * KG>(a, m0, n0, kt0, kt1, smem, compute);
+    if constexpr (mm_pipelined<WM, WN, BK, DB, KG>()) {
+        if (a.direct) mm_mfma_pipe<WM, WN, BK, UF, DB, KG>(a, m0, n0, kt0, kt1, smem, acc);
+        else k_loop<BM, BN, BK, ST, 256 * KG>(a, m0, n0, kt0, kt1, smem, compute);
+    } else {
+        k_loop<BM, BN, BK, ST, 256 * KG>(a, m0, n0, kt0, kt1, smem, compute);
+    }
 
     constexpr int NV = BIG ? 16 : 4;
     if constexpr (KG > 1) {

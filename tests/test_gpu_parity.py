@@ -156,6 +156,29 @@ def test_parity_bit_exact(torch_dev, lib, name, op, sh, kind):
         assert np.array_equal(y, ref), f"{name} {kind} {o.knobs(p)}"
 
 
+def test_matmul_every_mfma_class_exact(torch_dev, lib):
+    """One point of every MFMA matmul class (tile, K-tile, stages, split and
+    the two operand-prefetch depths) on an aligned shape, where full tiles take
+    the direct, software-pipelined path: bit-exact on small-integer inputs."""
+    sh = (256, 256, 512)
+    x, w = synthdata.matmul_inputs(sh, "int")
+    ref = ok.matmul_f64(x, w).ravel()
+    r = Runner(torch_dev, lib, 2, sh, x, w)
+    o = osp.Space(2, sh)
+    seen = set()
+    for p in o.valid_points():
+        k = o.knobs(p)
+        if k["mfma"] != 1:
+            continue
+        cls = (k["bm"], k["bn"], k["bk"], k["dbuf"], k["ks"], k["unroll"] >= 16)
+        if cls in seen:
+            continue
+        seen.add(cls)
+        y = r.run(p)
+        assert np.array_equal(y, ref), f"matmul {sh} int {k}"
+    assert len(seen) > 500
+
+
 def test_empty_batch_and_rows(torch_dev, lib):
     torch = torch_dev
     s = lib.Space(1, (0, 4, 8, 8, 4, 3, 3, 1, 1))
