@@ -189,8 +189,10 @@ def main(argv=None):
         roofline = {"bound": "mfma" if per_task[j]["best_schedule"].get("mfma", 0) else "alu",
                     "achieved": round(ach, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(ach / PEAK_FP32_TFLOPS, 4)}
+    geom = task["space"].geometry(res.best.index())
     roofline.update({"traffic": measured_traffic(kname, per_task[j]["best_schedule"]),
                      "kernel": kname, "task": task["name"],
+                     "grid_threads": int(geom["grid"]) * int(geom["threads"]),
                      "avg_launch_us": round(avg_ms * 1e3, 3),
                      "algorithmic_flops": task["flops"], "algorithmic_bytes": task["bytes"]})
 

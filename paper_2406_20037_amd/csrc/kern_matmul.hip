@@ -584,7 +584,8 @@ __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
 
     constexpr int NV = BIG ? 16 : 4;
     if constexpr (KG > 1) {
-        // group 1 hands its partial tile to group 0 through LDS
+        // group 1 hands its partial tile to group 0 through LDS (16 bytes
+        // per lane per access: value quad q of block b at ((b*NV/4 + q)*64 + lane)*4)
         __syncthreads();
         float *rb = smem + wq * (WM * WN);
         if (kg == 1) {
@@ -593,7 +594,10 @@ __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
 #pragma unroll
                 for (int j = 0; j < NB; ++j)
 #pragma unroll
-                    for (int v = 0; v < NV; ++v) rb[((i * NB + j) * NV + v) * 64 + lane] = acc[i][j][v];
+                    for (int q = 0; q < NV / 4; ++q)
+                        *reinterpret_cast<floatx4 *>(rb + (((i * NB + j) * (NV / 4) + q) * 64 + lane) * 4) =
+                            floatx4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                    acc[i][j][4 * q + 3]};
         }
         __syncthreads();
         if (kg == 1) return;
@@ -602,7 +606,12 @@ __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
 #pragma unroll
             for (int j = 0; j < NB; ++j)
 #pragma unroll
-                for (int v = 0; v < NV; ++v) acc[i][j][v] += rb[((i * NB + j) * NV + v) * 64 + lane];
+                for (int q = 0; q < NV / 4; ++q) {
+                    const floatx4 t = *reinterpret_cast<const floatx4 *>(
+                        rb + (((i * NB + j) * (NV / 4) + q) * 64 + lane) * 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += t[e];
+                }
     }
 
     // Output layout: 32x32 block, lane holds rows 8*(v/4) + 4*lg + v%4 of

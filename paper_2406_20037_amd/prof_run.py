@@ -4,8 +4,10 @@ profiling a single kernel instance with rocprofv3.
     python -m paper_2406_20037_amd.prof_run --workload matmul_1024 \
         --sched bm=64,bn=32,bk=32,unroll=64,dbuf=1,mfma=1,ks=2 --iters 100
 
-The copy (torch's elementwise copy of --copy-mib MiB) gives the factor that
-relates the HBM counters to bytes actually moved.
+The schedule is launched the way the tuner times it: --iters launches captured
+in a HIP graph and replayed back to back (--host-launch: one host launch per
+iteration instead).  The copy (torch's elementwise copy of --copy-mib MiB)
+gives the factor that relates the HBM counters to bytes actually moved.
 """
 from __future__ import annotations
 
@@ -24,6 +26,8 @@ def main(argv=None):
     ap.add_argument("--sched", required=True, help="knob=value,... (every axis)")
     ap.add_argument("--iters", type=int, default=100)
     ap.add_argument("--copy-mib", type=int, default=64)
+    ap.add_argument("--host-launch", action="store_true",
+                    help="launch from the host one by one instead of a replayed graph")
     args = ap.parse_args(argv)
 
     import torch
@@ -52,15 +56,23 @@ def main(argv=None):
         n_out = shape[0] * shape[1]
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     yd = torch.empty(n_out, device="cuda:0")
-    for _ in range(args.iters):
-        L.kernel_run(op, s, xd, wd, yd)
+    if args.host_launch:
+        for _ in range(args.iters):
+            L.kernel_run(op, s, xd, wd, yd)
+    else:
+        # a first and a warm-up launch, then a graph of --iters launches replayed
+        # twice (warm-up and timed repeat)
+        cfg = L.measure_cfg(warmup=1, repeat=1, min_repeat_ms=1e9, max_number=args.iters,
+                            check=0, graph=1)
+        L.ds_measure(s, L.make_io(xd, wd, yd, None, torch.cuda.current_stream()), cfg)
     n = args.copy_mib * (1 << 20) // 4
     a = torch.ones(n, device="cuda:0")
     b = torch.empty_like(a)
     for _ in range(args.iters):
         b.copy_(a)
     torch.cuda.synchronize()
-    print(f"ran {args.iters} x {space.knobs(s)} and {args.iters} x copy of {args.copy_mib} MiB",
+    launches = args.iters if args.host_launch else 2 * args.iters + 2
+    print(f"ran {launches} x {space.knobs(s)} and {args.iters} x copy of {args.copy_mib} MiB",
           flush=True)
 
 

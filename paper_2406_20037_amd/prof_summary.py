@@ -38,13 +38,26 @@ def source_hash(kernel: str) -> str | None:
     return None
 
 
+# Position of the unroll-factor template argument of each kernel family.
+UNROLL_ARG = {"mm_mfma": 3, "mm_valu": 3, "conv_mfma": 2, "conv_valu": 2}
+
+
 def traffic_key(kernel: str, sched: str) -> str:
     """Key of a kernel's HBM traffic entry: the instance and the schedule (the
-    same instance runs with different runtime tile arguments).  The unroll
-    knob is left out: it reaches the launch only through the instance's unroll
-    factor, which the instance name already carries."""
+    same instance runs with different runtime tile arguments).  The unroll knob
+    and the instance's unroll factor are left out: they order instructions and
+    set how far ahead operands are read, but never change the addresses a
+    launch reads or writes."""
+    name = kernel
+    if "<" in kernel and kernel.endswith(">"):
+        fam, args = kernel[:-1].split("<", 1)
+        parts = [a.strip() for a in args.split(",")]
+        pos = UNROLL_ARG.get(fam.strip())
+        if pos is not None and pos < len(parts):
+            parts[pos] = "*"
+        name = f"{fam}<{', '.join(parts)}>"
     kept = [kv for kv in sched.split(",") if kv and not kv.startswith("unroll=")]
-    return f"{kernel} {','.join(kept)}" if kept else kernel
+    return f"{name} {','.join(kept)}" if kept else name
 
 
 def short(name: str) -> str:
@@ -69,6 +82,35 @@ def counters(db):
     return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
 
 
+def bench_check(db, bench_json):
+    """The dominant kernel of a profiled bench.py run: its traced dispatches at
+    the tuned launch shape against the average launch time bench.py reported
+    (HIP events over back-to-back graph launches, so it also holds the gap
+    between consecutive kernels)."""
+    with open(bench_json) as fh:
+        line = [ln for ln in fh if ln.lstrip().startswith("{")][-1]
+    rf = json.loads(line)["roofline"]
+    kname, threads = rf["kernel"], rf.get("grid_threads")
+    cur = sqlite3.connect(db).cursor()
+    durs = [(d, g) for name, d, g in cur.execute(
+        "select name, duration, grid_x * grid_y * grid_z from kernels") if short(name) == kname]
+    at = sorted(d for d, g in durs if threads is None or g == threads)
+    print(f"\n### Dominant kernel of the profiled bench.py run\n")
+    print(f"bench.py: `{kname}` on task {rf['task']}, average launch {rf['avg_launch_us']:.3f} us "
+          f"(events over the timed graph launches), {rf['achieved']} {rf['unit']} "
+          f"= {rf['frac']:.3f} of {rf['peak']}.\n")
+    if not at:
+        print("No traced dispatch of that kernel at that launch shape.")
+        return
+    mean = sum(at) / len(at) / 1e3
+    med = at[len(at) // 2] / 1e3
+    print("| dispatches (this instance, this grid) | mean us | median us | min us | bench avg launch us "
+          "| bench - trace mean us |")
+    print("|---:|---:|---:|---:|---:|---:|")
+    print(f"| {len(at)} of {len(durs)} | {mean:.3f} | {med:.3f} | {at[0] / 1e3:.3f} | "
+          f"{rf['avg_launch_us']:.3f} | {rf['avg_launch_us'] - mean:.3f} |")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
@@ -83,6 +125,9 @@ def main(argv=None):
     ap.add_argument("--sched", default="",
                     help="schedule the profiled launches ran (knob=value,... in axis order); "
                          "--json-out entries are keyed by kernel and schedule")
+    ap.add_argument("--bench-json",
+                    help="bench.py output of the profiled run: compare its dominant kernel's "
+                         "average launch time with the traced dispatch durations")
     args = ap.parse_args(argv)
     rows, n = top_kernels(args.trace, args.top)
     print(f"### Kernel trace ({n} distinct kernels; top {len(rows)} by total time)\n")
@@ -90,6 +135,8 @@ def main(argv=None):
     print("|---|---:|---:|---:|---:|")
     for name, calls, tot, avg, pct in rows:
         print(f"| `{short(name)}` | {calls} | {tot:.1f} | {avg:.3f} | {pct:.1f} |")
+    if args.bench_json:
+        bench_check(args.trace, args.bench_json)
     if args.fetch and args.write:
         copy_bytes_kib = args.copy_mib * 1024.0
         f, fn = counters(args.fetch)
