@@ -242,39 +242,49 @@ __device__ __forceinline__ void build_stage_tables(const ConvArgs &a, int kt, in
 
 // dma_chunk driven by the tables: one table read and one copy per position;
 // positions that read zero are never written (both buffers are zeroed once).
+// A wave takes its positions kCopyBatch instructions at a time: the batch's
+// table reads are all issued before its first copy, so one LDS latency is
+// paid per batch rather than per copy.
+constexpr int kCopyBatch = 8;
+
+template <int BYTES>
+__device__ __forceinline__ void copy_from_table(const float *src, const int *tabv, int n,
+                                                float *dst) {
+    constexpr int W = BYTES / 4;   // floats per lane
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nwv = blockDim.x >> 6;
+    const int step = nwv * 64;
+    for (int base = wid * 64; base < n; base += kCopyBatch * step) {
+        int e[kCopyBatch];
+#pragma unroll
+        for (int u = 0; u < kCopyBatch; ++u) {
+            const int q = base + u * step + lane;
+            const int t = tabv[q < n ? q : 0];
+            e[u] = q < n ? t : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kCopyBatch; ++u) {
+            if (e[u] < 0) continue;
+            if constexpr (BYTES == 16)
+                __builtin_amdgcn_global_load_lds(DS_GLOBAL(src + e[u]),
+                                                 DS_LOCAL(dst + W * (base + u * step)), 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds(DS_GLOBAL(src + e[u]),
+                                                 DS_LOCAL(dst + W * (base + u * step)), 4, 0, 0);
+        }
+    }
+}
+
 __device__ __forceinline__ void dma_chunk_tab(const ConvArgs &a, int n, int kt, int c0,
                                               const int *wsrc, const int *xsrc, float *wt,
                                               float *xs) {
     const int RS = a.R * a.S;
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nwv = blockDim.x >> 6;
     const float *wb = a.w + (size_t)kt * a.tk * a.C * RS + (size_t)c0 * RS;
     const float *xb = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
     const int npw = a.tk * a.wrow;
-    if (a.w4) {
-        // 16 bytes per lane: one instruction fills 256 consecutive floats
-        const int ng = npw >> 2;
-        for (int base = wid * 64; base < ng; base += nwv * 64) {
-            const int q = base + lane;
-            const int e = q < ng ? wsrc[q] : -1;
-            if (e >= 0)
-                __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + e), DS_LOCAL(wt + 4 * base), 16, 0,
-                                                 0);
-        }
-    } else {
-        for (int base = wid * 64; base < npw; base += nwv * 64) {
-            const int p = base + lane;
-            const int e = p < npw ? wsrc[p] : -1;
-            if (e >= 0)
-                __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + e), DS_LOCAL(wt + base), 4, 0, 0);
-        }
-    }
-    const int nh = a.tc * a.hs * a.ws;
-    for (int base = wid * 64; base < nh; base += nwv * 64) {
-        const int p = base + lane;
-        const int e = p < nh ? xsrc[p] : -1;
-        if (e >= 0)
-            __builtin_amdgcn_global_load_lds(DS_GLOBAL(xb + e), DS_LOCAL(xs + base), 4, 0, 0);
-    }
+    // weights: 16 bytes per lane (one instruction fills 256 floats) when rows allow
+    if (a.w4) copy_from_table<16>(wb, wsrc, npw >> 2, wt);
+    else copy_from_table<4>(wb, wsrc, npw, wt);
+    copy_from_table<4>(xb, xsrc, a.tc * a.hs * a.ws, xs);
 }
 
 // LDS staging set-up of a workgroup: the offset tables and zeroed buffers for
@@ -302,6 +312,76 @@ __device__ __forceinline__ void stage_to(const ConvArgs &a, float *smem, int b, 
         stage_chunk(a, n, kt, pt, qt, c0, wt, xs);
     }
 }
+
+// Chunk staging with the copy sources held in registers: the tables are the
+// same for every chunk, so when a thread's share of a kind (weights, halo)
+// fits in kRegCopies entries it reads them once, after stage_init, and each
+// chunk's copies of that kind need no LDS read (a table read before every copy
+// left the copies waiting on LDS latency).  Thread t's u-th copy of a kind
+// fills position u*blockDim + t (wave-uniform destination per u).  A kind
+// that does not fit is copied from its LDS table; the channel tail and
+// workgroups of partial waves go through stage_to.
+constexpr int kRegCopies = 8;
+
+struct RegStage {
+    int w[kRegCopies], h[kRegCopies];
+    bool onw, onh;
+
+    __device__ __forceinline__ void init(const ConvArgs &a, const int *wsrc, const int *xsrc) {
+        const int nt = blockDim.x;
+        const int nw = a.w4 ? (a.tk * a.wrow) >> 2 : a.tk * a.wrow;
+        const int nh = a.tc * a.hs * a.ws;
+        onw = (nt & 63) == 0 && nw <= kRegCopies * nt;
+        onh = (nt & 63) == 0 && nh <= kRegCopies * nt;
+#pragma unroll
+        for (int u = 0; u < kRegCopies; ++u) {
+            const int q = u * nt + threadIdx.x;
+            w[u] = onw && q < nw ? wsrc[q] : -1;
+            h[u] = onh && q < nh ? xsrc[q] : -1;
+        }
+    }
+
+    __device__ __forceinline__ void to(const ConvArgs &a, float *smem, int b, int n, int kt, int pt,
+                                       int qt, int ci, const int *wsrc, const int *xsrc) const {
+        const int c0 = ci * a.tc;
+        if (!(onw || onh) || c0 + a.tc > a.C) {
+            stage_to(a, smem, b, n, kt, pt, qt, ci, wsrc, xsrc);
+            return;
+        }
+        float *wt = smem + b * a.buf;
+        float *xs = wt + a.tk * a.wrow;
+        const int RS = a.R * a.S;
+        const float *wb = a.w + (size_t)kt * a.tk * a.C * RS + (size_t)c0 * RS;
+        const float *xb = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
+        const int slot = threadIdx.x & ~63, nt = blockDim.x;
+        const int npw = a.tk * a.wrow;
+        if (!onw) {
+            if (a.w4) copy_from_table<16>(wb, wsrc, npw >> 2, wt);
+            else copy_from_table<4>(wb, wsrc, npw, wt);
+        } else if (a.w4) {
+#pragma unroll
+            for (int u = 0; u < kRegCopies; ++u)
+                if (w[u] >= 0)
+                    __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + w[u]),
+                                                     DS_LOCAL(wt + 4 * (u * nt + slot)), 16, 0, 0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < kRegCopies; ++u)
+                if (w[u] >= 0)
+                    __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + w[u]),
+                                                     DS_LOCAL(wt + u * nt + slot), 4, 0, 0);
+        }
+        if (!onh) {
+            copy_from_table<4>(xb, xsrc, a.tc * a.hs * a.ws, xs);
+        } else {
+#pragma unroll
+            for (int u = 0; u < kRegCopies; ++u)
+                if (h[u] >= 0)
+                    __builtin_amdgcn_global_load_lds(DS_GLOBAL(xb + h[u]),
+                                                     DS_LOCAL(xs + u * nt + slot), 4, 0, 0);
+        }
+    }
+};
 
 template <int KPT, int PPT, int UF, int LDS>
 __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
@@ -339,9 +419,11 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
     int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
     int *wsrc = tab + a.red, *xsrc = wsrc + a.tk * a.wrow;     // LDS staging tables
     build_table(a, tab, LDS);
+    RegStage rs;
     if (LDS) {
         stage_init(a, smem, kt, pt, qt, wsrc, xsrc);
-        stage_to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
+        rs.init(a, wsrc, xsrc);
+        rs.to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
     }
 
     const int RS = a.R * a.S;
@@ -351,7 +433,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         if (LDS) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
-            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+            if (ci + 1 < ci1) rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             const float *wg = wt + g * KPT * a.wrow;
@@ -449,9 +531,11 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
     int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
     int *wsrc = tab + a.red, *xsrc = wsrc + a.tk * a.wrow;     // LDS staging tables
     build_table(a, tab, LDS);
+    RegStage rs;
     if (LDS) {
         stage_init(a, smem, kt, pt, qt, wsrc, xsrc);
-        stage_to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
+        rs.init(a, wsrc, xsrc);
+        rs.to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
     }
 
     constexpr int UG = UF >= 4 ? UF / 4 : 1;   // 16-step groups unrolled
@@ -463,7 +547,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         if (LDS) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
-            if (ci + 1 < ci1) stage_to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+            if (ci + 1 < ci1) rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             {
