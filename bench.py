@@ -190,7 +190,7 @@ def main(argv=None):
                     "achieved": round(ach, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(ach / PEAK_FP32_TFLOPS, 4)}
     geom = task["space"].geometry(res.best.index())
-    roofline.update({"traffic": measured_traffic(kname, per_task[j]["best_schedule"]),
+    roofline.update({"traffic": measured_traffic(kname, per_task[j]["best_schedule"], task["shape"]),
                      "kernel": kname, "task": task["name"],
                      "grid_threads": int(geom["grid"]) * int(geom["threads"]),
                      "avg_launch_us": round(avg_ms * 1e3, 3),
@@ -269,18 +269,19 @@ def cold_time(L, task, best, stream, reps=11, flush_mb=512):
     return sorted(times)[reps // 2]
 
 
-def measured_traffic(kname, knobs):
-    """HBM bytes per launch of this kernel instance at this schedule from the
-    committed rocprofv3 counter runs (FETCH_SIZE and WRITE_SIZE, each scaled
-    by the same counter on a copy of known size), or None when that schedule
-    was not profiled or the kernel sources changed since."""
+def measured_traffic(kname, knobs, shape):
+    """HBM bytes per launch of this kernel instance at this schedule and
+    problem shape from the committed rocprofv3 counter runs (FETCH_SIZE and
+    WRITE_SIZE, each scaled by the same counter on a copy of known size), or
+    None when that schedule was not profiled or the kernel sources changed
+    since."""
     from paper_2406_20037_amd.prof_summary import source_hash, traffic_key
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         data = json.load(fh)
-    e = data.get(traffic_key(kname, ",".join(f"{k}={v}" for k, v in knobs.items())))
+    e = data.get(traffic_key(kname, ",".join(f"{k}={v}" for k, v in knobs.items()), shape))
     if not e or e.get("source_sha256") != source_hash(kname):
         return None
     return int(round(e["read_bytes"] + e["write_bytes"]))

@@ -42,12 +42,12 @@ def source_hash(kernel: str) -> str | None:
 UNROLL_ARG = {"mm_mfma": 3, "mm_valu": 3, "conv_mfma": 2, "conv_valu": 2}
 
 
-def traffic_key(kernel: str, sched: str) -> str:
+def traffic_key(kernel: str, sched: str, shape=None) -> str:
     """Key of a kernel's HBM traffic entry: the instance and the schedule (the
     same instance runs with different runtime tile arguments).  The unroll knob
     and the instance's unroll factor are left out: they order instructions and
     set how far ahead operands are read, but never change the addresses a
-    launch reads or writes."""
+    launch reads or writes.  The problem shape, when given, ends the key."""
     name = kernel
     if "<" in kernel and kernel.endswith(">"):
         fam, args = kernel[:-1].split("<", 1)
@@ -57,7 +57,10 @@ def traffic_key(kernel: str, sched: str) -> str:
             parts[pos] = "*"
         name = f"{fam}<{', '.join(parts)}>"
     kept = [kv for kv in sched.split(",") if kv and not kv.startswith("unroll=")]
-    return f"{name} {','.join(kept)}" if kept else name
+    key = f"{name} {','.join(kept)}" if kept else name
+    if shape:
+        key += " shape=" + ",".join(str(int(v)) for v in shape)
+    return key
 
 
 def short(name: str) -> str:
@@ -125,6 +128,8 @@ def main(argv=None):
     ap.add_argument("--sched", default="",
                     help="schedule the profiled launches ran (knob=value,... in axis order); "
                          "--json-out entries are keyed by kernel and schedule")
+    ap.add_argument("--shape", default="",
+                    help="problem shape of the profiled launches (comma-separated); ends the keys")
     ap.add_argument("--bench-json",
                     help="bench.py output of the profiled run: compare its dominant kernel's "
                          "average launch time with the traced dispatch durations")
@@ -161,7 +166,8 @@ def main(argv=None):
             k = short(name)
             sh = source_hash(k)
             if sh:
-                entries[traffic_key(k, args.sched)] = {"fetch_kib": fv, "write_kib": wv, "read_factor": ff,
+                shape = [int(v) for v in args.shape.split(",")] if args.shape else None
+                entries[traffic_key(k, args.sched, shape)] = {"fetch_kib": fv, "write_kib": wv, "read_factor": ff,
                               "write_factor": wf, "read_bytes": fv * ff * 1024,
                               "write_bytes": wv * wf * 1024, "source_sha256": sh,
                               "command": args.command}
