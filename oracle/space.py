@@ -241,7 +241,13 @@ def conv_geometry(shape, v):
         wrow = red + 4
         t0, t1 = tkb, npb           # template parameters: channel blocks, pixel blocks per wave
     hs = (th - 1) * st + R
-    ws = (tw - 1) * st + S
+    # aligned halo layout (image rows of whole 16-byte groups, tiles of at
+    # least 16 input columns): rows start at the 16-byte boundary at or before
+    # the tile's first column, up to 3 more columns, rounded to 4
+    if W % 4 == 0 and tw * st >= 16:
+        ws = _cdiv((tw - 1) * st + S + 3, 4) * 4
+    else:
+        ws = (tw - 1) * st + S
     chunks = max(1, _cdiv(C, tc))
     if v["lds"]:
         # weights + halo (+ one zero float) per buffer, rounded to 16 bytes; two

@@ -100,8 +100,12 @@ struct ConvArgs {
     int ltw;              // log2(tw)
     int nbuf, buf;        // LDS buffers (1 or 2) and floats per buffer (16-byte multiple)
     float *part;          // ks > 1: split z writes its partial output at part + z * N*K*P*Q
-    int w4;               // 1: weight rows staged with 16-byte copies (C*R*S, tc*R*S,
-                          //    wrow multiples of 4 and w 16-byte aligned)
+    int w4;               // bit 0: weight rows staged with 16-byte copies (C*R*S, tc*R*S,
+                          //    wrow multiples of 4 and w 16-byte aligned); bit 1: halo
+                          //    rows too (aligned layout, tk*wrow a multiple of 4, x
+                          //    16-byte aligned); bit 2: aligned halo layout (W a
+                          //    multiple of 4 and tw*st >= 16: rows start at the
+                          //    16-byte boundary at or before the tile's first column)
     FastDiv f_hw, f_ws, f_red, f_rs, f_s, f_wrow;   // divisions by hs*ws, ws, red, R*S, S, wrow
 };
 

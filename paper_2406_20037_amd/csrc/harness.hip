@@ -440,7 +440,13 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.red = g.red;
         a.wrow = mfma ? g.red + 4 : g.red;
         a.hs = (a.th - 1) * a.st + a.R;
-        a.ws = (a.tw - 1) * a.st + a.S;
+        // aligned halo layout when image rows are whole 16-byte groups and the
+        // tile is at least 16 columns wide: rows start at the 16-byte boundary
+        // at or before the tile's first column (up to 3 more columns, rounded
+        // to 4); otherwise rows hold exactly the tile's input columns
+        const bool halo16 = a.W % 4 == 0 && a.tw * a.st >= 16;
+        a.ws = halo16 ? int(cdiv64(int64_t(a.tw - 1) * a.st + a.S + 3, 4) * 4)
+                      : (a.tw - 1) * a.st + a.S;
         a.npx = a.th * a.tw;
         a.npl = std::min(a.npx, 256);
         a.ltw = log2_exact(a.tw);
@@ -450,8 +456,15 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.f_rs = make_fastdiv(a.R * a.S);
         a.f_s = make_fastdiv(a.S);
         a.f_wrow = make_fastdiv(a.wrow);
-        a.w4 = (a.C * a.R * a.S) % 4 == 0 && (a.tc * a.R * a.S) % 4 == 0 && a.wrow % 4 == 0 &&
-               reinterpret_cast<uintptr_t>(w) % 16 == 0;
+        // bit 0: weight rows staged 16 bytes per lane; bit 1: halo rows too;
+        // bit 2: aligned halo layout
+        a.w4 = ((a.C * a.R * a.S) % 4 == 0 && (a.tc * a.R * a.S) % 4 == 0 && a.wrow % 4 == 0 &&
+                reinterpret_cast<uintptr_t>(w) % 16 == 0 ? 1 : 0) |
+               (halo16 && (int64_t(a.tk) * a.wrow) % 4 == 0 &&
+                        reinterpret_cast<uintptr_t>(x) % 16 == 0
+                    ? 2
+                    : 0) |
+               (halo16 ? 4 : 0);
         a.nbuf = cdiv64(a.chunks, a.ks) > 1 ? 2 : 1;
         a.buf = int(cdiv64(int64_t(a.tk) * a.wrow + int64_t(a.tc) * a.hs * a.ws + 1, 4) * 4);
         plan.func = mfma ? conv_mfma_instance(g.t0, g.t1, g.unroll_eff, lds)

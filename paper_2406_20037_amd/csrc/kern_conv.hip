@@ -92,13 +92,25 @@ __device__ __forceinline__ bool weight_src(const ConvArgs &a, int kr, int c0, in
 // global-load latency is paid once per batch rather than once per element.
 constexpr int kBatch = 8;
 
+// Image column of LDS halo column 0: the tile's first input column, or, with
+// the aligned halo layout (w4 bit 2), the 16-byte boundary at or before it (so
+// halo rows can travel 16 bytes per lane).
+__device__ __forceinline__ int halo_x0(const ConvArgs &a, int qt) {
+    const int x0 = qt * a.tw * a.st - a.pd;
+    return a.w4 & 4 ? x0 - (x0 & 3) : x0;
+}
+// Column of the tile's first input column inside a halo row.
+__device__ __forceinline__ int halo_shift(const ConvArgs &a, int qt) {
+    return a.w4 & 4 ? (qt * a.tw * a.st - a.pd) & 3 : 0;
+}
+
 __device__ __forceinline__ void stage_chunk(const ConvArgs &a, int n, int kt, int pt, int qt,
                                             int c0, float *wt, float *xs) {
     const int RS = a.R * a.S;
     const int real = a.tc * RS;
     const int hw = a.hs * a.ws;
     const int nh = a.tc * hw;
-    const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
+    const int hy0 = pt * a.th * a.st - a.pd, hx0 = halo_x0(a, qt);
     const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
     const int nt = blockDim.x;
     for (int e0 = threadIdx.x; e0 < nh; e0 += kBatch * nt) {
@@ -176,7 +188,7 @@ __device__ __forceinline__ void dma_chunk(const ConvArgs &a, int n, int kt, int 
     }
     const int hw = a.hs * a.ws;
     const int nh = a.tc * hw;
-    const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
+    const int hy0 = pt * a.th * a.st - a.pd, hx0 = halo_x0(a, qt);
     const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
     for (int base = wid * 64; base < nh; base += nwv * 64) {
         const int p = base + lane;
@@ -216,7 +228,7 @@ __device__ __forceinline__ void build_stage_tables(const ConvArgs &a, int kt, in
     const int real = a.tc * RS;
     const int crs = a.C * RS;
     const int npw = a.tk * a.wrow;
-    if (a.w4) {
+    if (a.w4 & 1) {
         // 16-byte groups: a group of four positions is valid or not as a whole
         for (int q = threadIdx.x; q < (npw >> 2); q += blockDim.x) {
             const int p = q << 2;
@@ -231,12 +243,16 @@ __device__ __forceinline__ void build_stage_tables(const ConvArgs &a, int kt, in
     }
     const int hw = a.hs * a.ws;
     const int nh = a.tc * hw;
-    const int hy0 = pt * a.th * a.st - a.pd, hx0 = qt * a.tw * a.st - a.pd;
-    for (int p = threadIdx.x; p < nh; p += blockDim.x) {
+    const int hy0 = pt * a.th * a.st - a.pd, hx0 = halo_x0(a, qt);
+    // 16-byte groups when image rows allow (W % 4 == 0: a group starting at a
+    // multiple of 4 is inside a row or outside it as a whole)
+    const int gsz = a.w4 & 2 ? 4 : 1;
+    for (int q = threadIdx.x; q < nh / gsz; q += blockDim.x) {
+        const int p = q * gsz;
         const int c_l = fdiv(p, a.f_hw), rem = p - c_l * hw;
         const int hy = fdiv(rem, a.f_ws), hx = rem - hy * a.ws;
         const int gy = hy0 + hy, gx = hx0 + hx;
-        xsrc[p] = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W ? (c_l * a.H + gy) * a.W + gx : -1;
+        xsrc[q] = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W ? (c_l * a.H + gy) * a.W + gx : -1;
     }
 }
 
@@ -282,9 +298,10 @@ __device__ __forceinline__ void dma_chunk_tab(const ConvArgs &a, int n, int kt, 
     const float *xb = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
     const int npw = a.tk * a.wrow;
     // weights: 16 bytes per lane (one instruction fills 256 floats) when rows allow
-    if (a.w4) copy_from_table<16>(wb, wsrc, npw >> 2, wt);
+    if (a.w4 & 1) copy_from_table<16>(wb, wsrc, npw >> 2, wt);
     else copy_from_table<4>(wb, wsrc, npw, wt);
-    copy_from_table<4>(xb, xsrc, a.tc * a.hs * a.ws, xs);
+    if (a.w4 & 2) copy_from_table<16>(xb, xsrc, (a.tc * a.hs * a.ws) >> 2, xs);
+    else copy_from_table<4>(xb, xsrc, a.tc * a.hs * a.ws, xs);
 }
 
 // LDS staging set-up of a workgroup: the offset tables and zeroed buffers for
@@ -329,8 +346,8 @@ struct RegStage {
 
     __device__ __forceinline__ void init(const ConvArgs &a, const int *wsrc, const int *xsrc) {
         const int nt = blockDim.x;
-        const int nw = a.w4 ? (a.tk * a.wrow) >> 2 : a.tk * a.wrow;
-        const int nh = a.tc * a.hs * a.ws;
+        const int nw = a.w4 & 1 ? (a.tk * a.wrow) >> 2 : a.tk * a.wrow;
+        const int nh = a.w4 & 2 ? (a.tc * a.hs * a.ws) >> 2 : a.tc * a.hs * a.ws;
         onw = (nt & 63) == 0 && nw <= kRegCopies * nt;
         onh = (nt & 63) == 0 && nh <= kRegCopies * nt;
 #pragma unroll
@@ -356,9 +373,9 @@ struct RegStage {
         const int slot = threadIdx.x & ~63, nt = blockDim.x;
         const int npw = a.tk * a.wrow;
         if (!onw) {
-            if (a.w4) copy_from_table<16>(wb, wsrc, npw >> 2, wt);
+            if (a.w4 & 1) copy_from_table<16>(wb, wsrc, npw >> 2, wt);
             else copy_from_table<4>(wb, wsrc, npw, wt);
-        } else if (a.w4) {
+        } else if (a.w4 & 1) {
 #pragma unroll
             for (int u = 0; u < kRegCopies; ++u)
                 if (w[u] >= 0)
@@ -371,8 +388,16 @@ struct RegStage {
                     __builtin_amdgcn_global_load_lds(DS_GLOBAL(wb + w[u]),
                                                      DS_LOCAL(wt + u * nt + slot), 4, 0, 0);
         }
+        const int nh = a.tc * a.hs * a.ws;
         if (!onh) {
-            copy_from_table<4>(xb, xsrc, a.tc * a.hs * a.ws, xs);
+            if (a.w4 & 2) copy_from_table<16>(xb, xsrc, nh >> 2, xs);
+            else copy_from_table<4>(xb, xsrc, nh, xs);
+        } else if (a.w4 & 2) {
+#pragma unroll
+            for (int u = 0; u < kRegCopies; ++u)
+                if (h[u] >= 0)
+                    __builtin_amdgcn_global_load_lds(DS_GLOBAL(xb + h[u]),
+                                                     DS_LOCAL(xs + 4 * (u * nt + slot)), 16, 0, 0);
         } else {
 #pragma unroll
             for (int u = 0; u < kRegCopies; ++u)
@@ -404,7 +429,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         const int py = pix >> a.ltw, px = pix & (a.tw - 1);
         const int p = pt * a.th + py, q = qt * a.tw + px;
         pv[j] = pix < a.npx && p < a.P && q < a.Q;
-        poff[j] = py * a.st * a.ws + px * a.st;
+        poff[j] = py * a.st * a.ws + px * a.st + halo_shift(a, qt);
         iy0[j] = p * a.st - a.pd;
         ix0[j] = q * a.st - a.pd;
         oq[j] = p * a.Q + q;
@@ -516,7 +541,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         const int py = pix >> a.ltw, px = pix & (a.tw - 1);
         const int p = pt * a.th + py, q = qt * a.tw + px;
         pv[b] = pix < a.npx && p < a.P && q < a.Q;
-        poff[b] = py * a.st * a.ws + px * a.st;
+        poff[b] = py * a.st * a.ws + px * a.st + halo_shift(a, qt);
         iy0[b] = p * a.st - a.pd;
         ix0[b] = q * a.st - a.pd;
         oq[b] = p * a.Q + q;

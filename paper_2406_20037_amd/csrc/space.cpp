@@ -109,7 +109,12 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         g.t0 = tkb;
         g.t1 = npb;
     }
-    const int64_t hs = int64_t(th - 1) * st + R, ws = int64_t(tw - 1) * st + S;
+    // aligned halo layout (image rows of whole 16-byte groups, tiles of at
+    // least 16 input columns): rows start at the 16-byte boundary at or before
+    // the tile's first column, up to 3 more columns, rounded to 4
+    const bool halo16 = W % 4 == 0 && int64_t(tw) * st >= 16;
+    const int64_t hs = int64_t(th - 1) * st + R;
+    const int64_t ws = halo16 ? cdiv(int64_t(tw - 1) * st + S + 3, 4) * 4 : int64_t(tw - 1) * st + S;
     g.chunks = std::max<int64_t>(1, cdiv(C, tc));
     int64_t lds_bytes;
     if (lds) {

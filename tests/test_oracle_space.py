@@ -77,10 +77,10 @@ def test_conv_geometry_hand_computed():
     s = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
     g = s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1))
     # 64 pixels -> one 16-pixel block per wave; 16 channels -> one block.
-    # reduction 16*9 = 144; halo 10x10; LDS 4*(16*100+1) + 4*16*144 + 4*144.
-    # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148; 4 chunks
-    # in one split -> two buffers of 16*148 + 16*100 + 1 -> 3972 floats, + table,
-    # + one staging source per weight and halo position (2368 + 1600).
+    # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148; halo
+    # 10x10 (8 columns wide: no aligned layout); 4 chunks in one split -> two
+    # buffers of 16*148 + 16*100 + 1 -> 3972 floats, + table, + one staging
+    # source per weight and halo position (2368 + 1600).
     assert g == dict(valid=True, grid=4 * 7 * 7, threads=256,
                      lds_bytes=4 * (2 * 3972 + 144 + 2368 + 1600), acc=4,
                      unroll_eff=16, t0=1, t1=1, red=144, chunks=4)
@@ -96,19 +96,22 @@ def test_conv_geometry_hand_computed():
     # Fewer than 64 outputs: not a full wave.
     assert not s.valid(idx_of(s, tk=2, th=4, tw=4, tc=1, unroll=0, lds=0, ks=1, mfma=0))
     # MFMA reduction padded to a multiple of 16: 4 channels x 9 taps = 36 -> 48;
-    # 16 chunks -> two buffers of 32*52 + 4*6*18 + 1 = 2097 -> 2100 floats.
+    # 16 columns wide on an image of 56 (a multiple of 4): aligned halo layout,
+    # rows of 18 + 3 -> 24 floats; 16 chunks -> two buffers of
+    # 32*52 + 4*6*24 + 1 = 2241 -> 2244 floats.
     g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1))
-    assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2100 + 48 + 1664 + 432)
+    assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2244 + 48 + 1664 + 576)
     # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
     assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
     # MFMA needs >= 16 channels and >= 16 pixels (one 16x16 block per wave).
     assert not s.valid(idx_of(s, tk=8, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
     assert not s.valid(idx_of(s, tk=16, th=2, tw=4, tc=4, unroll=0, lds=0, ks=1, mfma=1))
     assert s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
-    # LDS limit: 64-channel chunk of a 34x34 halo does not fit (one chunk, one
-    # buffer of 16*576 + 64*34*34 + 1 -> 83204 floats).
+    # LDS limit: 64-channel chunk of a 34-row halo in the aligned layout (rows
+    # of 34 + 3 -> 40 floats) does not fit (one chunk, one buffer of
+    # 16*576 + 64*34*40 + 1 -> 96260 floats).
     g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0))
-    assert g["lds_bytes"] == 4 * (83204 + 576 + 9216 + 73984) and not g["valid"]
+    assert g["lds_bytes"] == 4 * (96260 + 576 + 9216 + 87040) and not g["valid"]
     # split finer than the chunk count.
     assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0))
 
