@@ -179,6 +179,44 @@ def test_matmul_every_mfma_class_exact(torch_dev, lib):
     assert len(seen) > 500
 
 
+@pytest.mark.parametrize("shift_x,shift_w", [(1, 0), (0, 1), (1, 1)])
+def test_parity_misaligned_operands(torch_dev, lib, shift_x, shift_w):
+    """Operands that start 4 bytes past a 16-byte boundary: the 16-byte staging
+    copies (weights, aligned halo rows, direct matmul tiles) must give way to
+    the 4-byte ones without changing the result.  Small-integer inputs, so
+    every schedule must match the oracle exactly."""
+    torch = torch_dev
+
+    def shifted(a, k):
+        buf = torch.zeros(a.size + k, dtype=torch.float32, device="cuda:0")
+        buf[k:] = torch.from_numpy(np.ascontiguousarray(a).ravel()).to("cuda:0")
+        return buf[k:]
+
+    cases = [(1, (1, 64, 56, 56, 64, 3, 3, 1, 1)), (1, (1, 3, 224, 224, 64, 7, 7, 2, 3)),
+             (2, (256, 256, 512))]
+    for op, sh in cases:
+        if op == 1:
+            x, w = synthdata.conv_inputs(sh, "int")
+            ref = ok.conv2d_f64(x, w, sh).ravel()
+        else:
+            x, w = synthdata.matmul_inputs(sh, "int")
+            ref = ok.matmul_f64(x, w).ravel()
+        xd, wd = shifted(x, shift_x), shifted(w, shift_w)
+        assert (xd.data_ptr() % 16 == 0) == (shift_x == 0)
+        n = out_elems(op, sh)
+        y = torch.empty(n, dtype=torch.float32, device="cuda:0")
+        space = lib.Space(op, sh)
+        o = osp.Space(op, sh)
+        pts = [p for p in pick_points(o, 60, seed=11, per_value=1)
+               if o.knobs(p).get("lds", 1) == 1 or op == 2]
+        for p in pts:
+            y.fill_(float("nan"))
+            lib.kernel_run(op, space.sched(p), xd, wd, y)
+            torch.cuda.synchronize()
+            out = y.cpu().numpy().astype(np.float64)
+            assert np.array_equal(out, ref), f"{sh} shift x {shift_x} w {shift_w} {o.knobs(p)}"
+
+
 def test_empty_batch_and_rows(torch_dev, lib):
     torch = torch_dev
     s = lib.Space(1, (0, 4, 8, 8, 4, 3, 3, 1, 1))
