@@ -458,7 +458,14 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         if (LDS) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
-            if (ci + 1 < ci1) rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+            if (ci + 1 < ci1) {
+                // the copies are issued at raised wave priority: next to waves
+                // that issue MFMAs back to back their vector instructions
+                // otherwise wait for issue slots
+                __builtin_amdgcn_s_setprio(3);
+                rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+                __builtin_amdgcn_s_setprio(0);
+            }
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             const float *wg = wt + g * KPT * a.wrow;
@@ -572,7 +579,14 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         if (LDS) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
-            if (ci + 1 < ci1) rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+            if (ci + 1 < ci1) {
+                // the copies are issued at raised wave priority: next to waves
+                // that issue MFMAs back to back their vector instructions
+                // otherwise wait for issue slots
+                __builtin_amdgcn_s_setprio(3);
+                rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+                __builtin_amdgcn_s_setprio(0);
+            }
             const float *wt = smem + bi * a.buf;
             const float *xs = wt + a.tk * a.wrow;
             {
