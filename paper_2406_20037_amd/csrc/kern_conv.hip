@@ -443,6 +443,8 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
 
     int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
     int *wsrc = tab + a.red, *xsrc = wsrc + a.tk * a.wrow;     // LDS staging tables
+    // the set-up and the first copies also run at raised priority
+    __builtin_amdgcn_s_setprio(3);
     build_table(a, tab, LDS);
     RegStage rs;
     if (LDS) {
@@ -450,6 +452,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
         rs.init(a, wsrc, xsrc);
         rs.to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
     }
+    __builtin_amdgcn_s_setprio(0);
 
     const int RS = a.R * a.S;
     const int crs = a.C * RS;
@@ -562,6 +565,8 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
 
     int *tab = LDS ? reinterpret_cast<int *>(smem + a.nbuf * a.buf) : reinterpret_cast<int *>(smem);
     int *wsrc = tab + a.red, *xsrc = wsrc + a.tk * a.wrow;     // LDS staging tables
+    // the set-up and the first copies also run at raised priority
+    __builtin_amdgcn_s_setprio(3);
     build_table(a, tab, LDS);
     RegStage rs;
     if (LDS) {
@@ -569,6 +574,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         rs.init(a, wsrc, xsrc);
         rs.to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
     }
+    __builtin_amdgcn_s_setprio(0);
 
     constexpr int UG = UF >= 4 ? UF / 4 : 1;   // 16-step groups unrolled
     const int RS = a.R * a.S;
