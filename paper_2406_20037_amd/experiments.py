@@ -6,6 +6,7 @@ object per result line on stdout and progress on stderr.
     python -m paper_2406_20037_amd.experiments exploiters --workload matmul_1024 --seeds 3
     python -m paper_2406_20037_amd.experiments sweep --workload conv3x3_c64_56 --seeds 3
     python -m paper_2406_20037_amd.experiments tasks --workload resnet50 --trials 24,300,1000
+    python -m paper_2406_20037_amd.experiments report out/*.jsonl
 
 Every reported kernel time is re-measured with 31 repeats (graph replays) so
 that strategies are compared on one footing; tuning-time figures are the
@@ -22,6 +23,7 @@ import time
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
+BEST = "best_us"
 KIND_NAMES = {0: "droplet", 1: "random", 2: "grid", 3: "ga"}
 CONFIG_OF = {"conv3x3_c64_56": 0, "matmul_1024": 1, "conv7x7_s2_c3_224": 2}
 
@@ -168,9 +170,74 @@ def run_tasks(L, args, stream):
         emit(row)
 
 
+def _mean(v):
+    return sum(v) / len(v)
+
+
+def report(paths):
+    """Markdown tables over the JSON lines the three experiments print."""
+    rows = []
+    for p in paths:
+        with open(p) as fh:
+            rows += [json.loads(line) for line in fh if line.strip()]
+    out = []
+    ex = [r for r in rows if r["experiment"] == "exploiters"]
+    for wl in dict.fromkeys(r["workload"] for r in ex):
+        rs = [r for r in ex if r["workload"] == wl]
+        seeds = list(dict.fromkeys(r["seed"] for r in rs))
+        seed_us = [next(r["seed_us"] for r in rs if r["seed"] == s) for s in seeds]
+        out.append(f"{wl}: {len(seeds)} seeds, best of {rs[0]['n_explore']} samples "
+                   f"{_mean(seed_us):.2f} us (mean)\n")
+        out.append("| strategy | invalid points | best us (mean) | per seed | trials | failed | "
+                   "exploit s |")
+        out.append("|---|---|---:|---|---|---|---|")
+        for strat in dict.fromkeys((r["strategy"], r["valid_only"]) for r in rs):
+            g = [r for r in rs if (r["strategy"], r["valid_only"]) == strat]
+            out.append(
+                f"| {strat[0]} | {'skipped' if strat[1] else 'count'} | "
+                f"{_mean([r['best_us'] for r in g]):.2f} | "
+                f"{' / '.join(f'{r[BEST]:.2f}' for r in g)} | "
+                f"{' / '.join(str(r['measured']) for r in g)} | "
+                f"{' / '.join(str(r['failed']) for r in g)} | "
+                f"{_mean([r['exploit_s'] for r in g]):.2f} |")
+        out.append("")
+    sw = [r for r in rows if r["experiment"] == "sweep"]
+    for wl in dict.fromkeys(r["workload"] for r in sw):
+        rs = [r for r in sw if r["workload"] == wl]
+        out.append(f"{wl}: exploration budget N, then Droplet from the best sample\n")
+        out.append("| N | best us per seed | mean | Droplet trials per seed | explore s | "
+                   "Droplet s |")
+        out.append("|---:|---|---:|---|---:|---:|")
+        for n in sorted(dict.fromkeys(r["n_explore"] for r in rs)):
+            g = [r for r in rs if r["n_explore"] == n]
+            name = f"{n} (random only, {g[0]['n_explore_measured']} points)" \
+                if g[0].get("random_only") else str(n)
+            out.append(
+                f"| {name} | {' / '.join(f'{r[BEST]:.2f}' for r in g)} | "
+                f"{_mean([r['best_us'] for r in g]):.2f} | "
+                f"{' / '.join(str(r['n_droplet_measured']) for r in g)} | "
+                f"{_mean([r['explore_s'] for r in g]):.2f} | "
+                f"{_mean([r.get('droplet_s', 0.0) for r in g]):.2f} |")
+        out.append("")
+    ts = [r for r in rows if r["experiment"] == "tasks"]
+    for wl in dict.fromkeys(r["workload"] for r in ts):
+        rs = [r for r in ts if r["workload"] == wl]
+        out.append(f"{wl}: {len(rs[0]['per_task'])} tasks, network time = weighted sum of the "
+                   "re-measured per-task best\n")
+        out.append("| total exploration trials | first-round quota | rounds | Droplet trials | "
+                   "network us | wall s |")
+        out.append("|---:|---:|---:|---:|---:|---:|")
+        for r in rs:
+            out.append(f"| {r['total_trials']} | {r['quota']} | {r['rounds']} | "
+                       f"{r['droplet_trials']} | {r['network_us']:.1f} | {r['wall_s']:.1f} |")
+        out.append("")
+    return "\n".join(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
-    ap.add_argument("experiment", choices=["exploiters", "sweep", "tasks"])
+    ap.add_argument("experiment", choices=["exploiters", "sweep", "tasks", "report"])
+    ap.add_argument("files", nargs="*", help="report: JSON-lines files the experiments wrote")
     ap.add_argument("--workload", default="matmul_1024")
     ap.add_argument("--seeds", type=int, default=3)
     ap.add_argument("--n-explore", type=int, default=300)
@@ -179,6 +246,9 @@ def main(argv=None):
     ap.add_argument("--random-10k", action="store_true")
     ap.add_argument("--trials", default="24,300,1000,2400")
     args = ap.parse_args(argv)
+    if args.experiment == "report":
+        print(report(args.files))
+        return 0
 
     import torch
 
