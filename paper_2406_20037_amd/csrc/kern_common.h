@@ -19,10 +19,11 @@ __device__ __forceinline__ int xcd_tile(int b, int nwg) {
     return x * q + (x < r ? x : r) + j;
 }
 
-// Matmul output stores carry the non-temporal hint: no kernel reads its own
-// outputs back, and for whole 128-byte row segments it shortens the time from
-// one launch to the next by 1-2% (measured at 1024^3); the convolutions' partly
-// coalesced output stores run slower with it, so they store normally.
+// Output store with the non-temporal hint.  The matmul's 32x32-block epilogue
+// uses it: no kernel reads its own outputs back, and for whole 128-byte row
+// segments it shortens the time from one launch to the next by 1-2% (measured
+// at 1024^3).  Partly coalesced stores (the convolutions', 64-byte segments)
+// run slower or write more with it and store normally.
 __device__ __forceinline__ void store_out(float *p, float v) { __builtin_nontemporal_store(v, p); }
 
 // Instance table sizes (one slot per template-parameter tuple).

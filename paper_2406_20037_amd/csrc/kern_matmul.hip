@@ -311,7 +311,7 @@ __global__ __launch_bounds__(256) void mm_valu(MatmulArgs a) {
 #pragma unroll
         for (int j = 0; j < RN; ++j) {
             const int gn = n0 + tx * RN + j;
-            if (gn < a.N) store_out(crow + gn, acc[i][j]);
+            if (gn < a.N) crow[gn] = acc[i][j];
         }
     }
 }
@@ -628,7 +628,12 @@ __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
                 const int row = BIG ? 8 * (v / 4) + 4 * lg + (v % 4) : 4 * lg + v;
                 const int gm = m0 + wr * WM + i * IM + row;
                 if (gm >= a.M) continue;
-                store_out(cbase + (size_t)gm * a.N + gn, acc[i][j][v]);
+                // 32x32 blocks write whole 128-byte row segments per half-wave:
+                // those go out with the non-temporal hint; the 64-byte segments of
+                // 16x16 blocks stay in L2 to be merged (with the hint they cost
+                // up to 1.5x the HBM writes)
+                if constexpr (BIG) store_out(cbase + (size_t)gm * a.N + gn, acc[i][j][v]);
+                else cbase[(size_t)gm * a.N + gn] = acc[i][j][v];
             }
         }
 }
