@@ -342,8 +342,14 @@ enum {
     DS_EXPLOIT_DROPLET = 0,  /* Droplet Search (Section 2.2): converges, at most budget trials */
     DS_EXPLOIT_RANDOM = 1,   /* independent uniform draws of each axis index */
     DS_EXPLOIT_GRID = 2,     /* mixed-radix walk key(start)+1, +2, ... (first axis fastest) */
-    DS_EXPLOIT_GA = 3        /* genetic algorithm: elitism, roulette selection by 1/time,
+    DS_EXPLOIT_GA = 3,       /* genetic algorithm: elitism, roulette selection by 1/time,
                                 one-point crossover, per-gene mutation */
+    DS_EXPLOIT_DROPLET_LINE = 4  /* Droplet Search with line steps: after each move along
+                                    one axis, keep stepping that way (one charged trial per
+                                    step) while the step is valid and better, then scan the
+                                    neighbourhood again (the paper calls Droplet a line search
+                                    and presents it without its speculative steps, Section
+                                    2.2; this is one reading of those steps) */
 };
 
 typedef struct {

@@ -29,6 +29,17 @@ Readings taken where the paper is silent or loose:
   measurement has infinite time and still counts.
 * ``frozen`` lists axes that are held at the start's value (the single-sketch
   variant of Section 2.2's first limitation).
+* ``line`` (not the method of the paper's experiments): Section 2.2 presents
+  Droplet Search without the speculative steps of its original description
+  and calls it a line search; the reading taken for those steps is that a move
+  along axis a in direction d is followed by further steps along (a, d), each
+  a charged trial, for as long as the next point is in range, valid and better
+  than the current one.  The neighbourhood scan then resumes from the last
+  point reached.
+
+Pins of ``line`` (tests/test_oracle_droplet.py): a trace worked by hand on a
+separable 5x5 bowl, exhaustive search on convex costs, fewer trials than the
+plain search on long one-axis descents.
 
 Pins (tests/test_oracle_droplet.py): a trace worked by hand on the lattice of
 Example 3 (tests/golden/droplet_trace_example3.txt), exhaustive search on small
@@ -114,7 +125,7 @@ def better(a: Meas, b: Meas, alpha: float) -> bool:
     return ranksum_p_less(a.repeats, b.repeats) < alpha
 
 
-def droplet(space, cost, start=None, budget=100, alpha=1.0, cache=None, frozen=()):
+def droplet(space, cost, start=None, budget=100, alpha=1.0, cache=None, frozen=(), line=False):
     """Returns dict(best, meas, measured, status, path, order).
 
     ``cost(idx)`` returns a float, a list of repeat times, or a Meas.
@@ -155,10 +166,32 @@ def droplet(space, cost, start=None, budget=100, alpha=1.0, cache=None, frozen=(
         for nb in nbs:
             if best_nb is None or cache[space.key(nb)].median < cache[space.key(best_nb)].median:
                 best_nb = nb
-        if better(cache[space.key(best_nb)], cache[space.key(cur)], alpha):
-            cur = best_nb
+        if not better(cache[space.key(best_nb)], cache[space.key(cur)], alpha):
+            break
+        axis = next(a for a in range(len(cur)) if best_nb[a] != cur[a])
+        step = best_nb[axis] - cur[axis]
+        cur = best_nb
+        path.append(cur)
+        while line:
+            nxt = list(cur)
+            nxt[axis] += step
+            nxt = tuple(nxt)
+            if not 0 <= nxt[axis] < space.sizes[axis] or not space.valid(nxt):
+                break
+            kn = space.key(nxt)
+            if kn not in cache:
+                if nb_measured >= budget:
+                    status = EBUDGET
+                    stop = True
+                    break
+                cache[kn] = Meas.of(cost(nxt))
+                nb_measured += 1
+                order.append(kn)
+            if not better(cache[kn], cache[space.key(cur)], alpha):
+                break
+            cur = nxt
             path.append(cur)
-        else:
+        if stop:
             break
     return dict(best=cur, meas=cache[space.key(cur)], measured=start_measured + nb_measured,
                 status=status, path=path, order=order)

@@ -121,6 +121,7 @@ class ds_round(C.Structure):
 
 
 DS_EXPLOIT_DROPLET, DS_EXPLOIT_RANDOM, DS_EXPLOIT_GRID, DS_EXPLOIT_GA = 0, 1, 2, 3
+DS_EXPLOIT_DROPLET_LINE = 4
 
 # name -> (restype, argtypes); the list is also the set of exported symbols
 SIGNATURES = {

@@ -124,10 +124,14 @@ struct DropletOut {
     int status = DS_OK;
 };
 
-// Droplet Search from `start` over the cached measurements `cache`.
+// Droplet Search from `start` over the cached measurements `cache`.  With
+// `line`, every move along one axis is followed by steps further along that
+// axis in the same direction, one charged trial each, while a step is valid and
+// better; the neighbourhood scan then resumes from where the steps stopped.
 DropletOut droplet(const Space &sp, const int32_t *start, int budget, double alpha,
                    uint32_t frozen, std::unordered_map<uint64_t, Meas> &cache,
-                   const MeasureFn &measure, double &best_so_far, ds_trace *trace) {
+                   const MeasureFn &measure, double &best_so_far, ds_trace *trace,
+                   bool line = false) {
     DropletOut out;
     std::vector<int32_t> cur(start, start + sp.nknobs);
     uint64_t kcur = sp.key(cur.data());
@@ -176,13 +180,40 @@ DropletOut droplet(const Space &sp, const int32_t *start, int budget, double alp
         for (size_t i = 1; i < nbs.size(); ++i)
             if (cache[sp.key(nbs[i].data())].median < cache[sp.key(nbs[b].data())].median) b = i;
         const Meas &mb = cache[sp.key(nbs[b].data())];
-        if (better(mb, cache[kcur], alpha)) {
-            cur = nbs[b];
-            kcur = sp.key(cur.data());
+        if (!better(mb, cache[kcur], alpha)) break;
+        int axis = 0;
+        while (nbs[b][axis] == cur[axis]) ++axis;
+        const int dir = nbs[b][axis] - cur[axis];
+        cur = nbs[b];
+        kcur = sp.key(cur.data());
+        out.moves++;
+        while (line) {
+            const int j = cur[axis] + dir;
+            if (j < 0 || j >= int(sp.values[axis].size())) break;
+            nb = cur;
+            nb[axis] = j;
+            if (!sp.geometry(nb.data()).valid) break;
+            const uint64_t k = sp.key(nb.data());
+            if (!cache.count(k)) {
+                if (nb_measured >= budget) {
+                    out.status = DS_EBUDGET;
+                    stop = true;
+                    break;
+                }
+                Meas m = measure(nb.data(), best_so_far);
+                if (m.status != DS_OK) out.failed++;
+                else best_so_far = best_so_far > 0 ? std::min(best_so_far, m.median) : m.median;
+                cache[k] = m;
+                nb_measured++;
+                out.measured++;
+                trace_push(trace, 2, m, k);
+            }
+            if (!better(cache[k], cache[kcur], alpha)) break;
+            cur = nb;
+            kcur = k;
             out.moves++;
-        } else {
-            break;
         }
+        if (stop) break;
     }
     out.best = cur;
     out.meas = cache[kcur];
@@ -774,7 +805,7 @@ int ds_exploit(const ds_space *space, const ds_sched *start, const ds_exploit_cf
     ds_tune_cfg tcfg;
     if (tcfg_in) tcfg = *tcfg_in;
     else ds_tune_cfg_default(&tcfg);
-    if (cfg.kind < DS_EXPLOIT_DROPLET || cfg.kind > DS_EXPLOIT_GA || cfg.budget < 0 ||
+    if (cfg.kind < DS_EXPLOIT_DROPLET || cfg.kind > DS_EXPLOIT_DROPLET_LINE || cfg.budget < 0 ||
         (cfg.kind == DS_EXPLOIT_GA &&
          (cfg.pop < 2 || cfg.elite < 0 || cfg.elite >= cfg.pop || !(cfg.mutation >= 0.0)))) {
         set_error("bad exploitation settings");
@@ -805,9 +836,10 @@ int ds_exploit(const ds_space *space, const ds_sched *start, const ds_exploit_cf
     double best_so_far = 0.0;
     for (const auto &kv : c) note_best(best_so_far, kv.second);
     const double t0 = now_s();
-    if (cfg.kind == DS_EXPLOIT_DROPLET) {
+    if (cfg.kind == DS_EXPLOIT_DROPLET || cfg.kind == DS_EXPLOIT_DROPLET_LINE) {
         const DropletOut d = droplet(sp, st.data(), cfg.budget, tcfg.alpha, tcfg.frozen_mask, c,
-                                     measure, best_so_far, trace);
+                                     measure, best_so_far, trace,
+                                     cfg.kind == DS_EXPLOIT_DROPLET_LINE);
         fill_result(res, sp, d);
         res->n_droplet_measured = d.measured;
         res->n_failed = d.failed;

@@ -1,5 +1,6 @@
 """Experiment drivers over the C ABI (no oracle, no CPU fallback): the
-exploitation-strategy comparison (Section 3, RQ4), the exploration-budget sweep
+exploitation-strategy comparison (Section 3, RQ4; Droplet Search, its variant
+with line steps, Random, Grid and GA), the exploration-budget sweep
 (RQ5) and the whole-network trial split (Section 2.1).  Each prints one JSON
 object per result line on stdout and progress on stderr.
 
@@ -24,7 +25,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
 BEST = "best_us"
-KIND_NAMES = {0: "droplet", 1: "random", 2: "grid", 3: "ga"}
+KIND_NAMES = {0: "droplet", 1: "random", 2: "grid", 3: "ga", 4: "droplet-line"}
 CONFIG_OF = {"conv3x3_c64_56": 0, "matmul_1024": 1, "conv7x7_s2_c3_224": 2}
 
 
@@ -82,8 +83,8 @@ def run_exploiters(L, args, stream):
         seed_us = task.retime_us(start)
         log(f"seed {seed}: explored {ex.n_explore_measured} in {ex.explore_s:.1f} s, best "
             f"{task.space.knobs(start)} {seed_us:.2f} us")
-        for kind in (0, 1, 2, 3):
-            for valid_only in ((0,) if kind == 0 else (0, 1)):
+        for kind in (0, 4, 1, 2, 3):
+            for valid_only in ((0,) if kind in (0, 4) else (0, 1)):
                 ecfg = L.exploit_cfg(kind=kind, budget=args.budget, seed=seed + 1,
                                      valid_only=valid_only)
                 res, _ = L.ds_exploit(task.space, start, ecfg, L.tune_cfg(), task.io,

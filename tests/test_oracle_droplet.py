@@ -72,8 +72,82 @@ def test_exhaustive_convex_every_start(seed):
         assert res["best"] == gmin
 
 
+def bowl(p):
+    return (p[0] - 4) ** 2 + (p[1] - 4) ** 2
+
+
+def test_line_hand_trace():
+    # Worked by hand on a 5x5 lattice, cost (i-4)^2 + (j-4)^2, start (0,0): the
+    # first scan measures (1,0) and (0,1) (both 25) and moves to the first;
+    # steps along +i measure (2,0) 20, (3,0) 17, (4,0) 16 and stop at the edge;
+    # the scan of (4,0) measures (4,1) 9 and moves; steps along +j measure
+    # (4,2) 4, (4,3) 1, (4,4) 0; the scan of (4,4) measures (3,4) 1 and stops.
+    lat = sp.Lattice([list(range(5)), list(range(5))])
+    calls = []
+
+    def cost(p):
+        calls.append(tuple(p))
+        return bowl(p)
+
+    res = dr.droplet(lat, cost, start=(0, 0), line=True)
+    assert calls == [(0, 0), (1, 0), (0, 1), (2, 0), (3, 0), (4, 0), (4, 1), (4, 2), (4, 3),
+                     (4, 4), (3, 4)]
+    assert res["path"] == [(0, 0), (1, 0), (2, 0), (3, 0), (4, 0), (4, 1), (4, 2), (4, 3),
+                           (4, 4)]
+    assert res["measured"] == 11 and res["best"] == (4, 4) and res["status"] == dr.OK
+    plain = dr.droplet(lat, bowl, start=(0, 0))
+    assert plain["best"] == (4, 4) and plain["measured"] > res["measured"]
+
+
+def test_line_budget_stops_inside_a_line():
+    lat = sp.Lattice([list(range(5)), list(range(5))])
+    res = dr.droplet(lat, bowl, start=(0, 0), budget=3, line=True)
+    # (1,0) and (0,1) by the scan, (2,0) by the first step; the next step is over budget
+    assert res["status"] == dr.EBUDGET and res["measured"] == 4 and res["best"] == (2, 0)
+
+
+def test_line_stops_at_invalid_points_and_worse_steps():
+    # (3,0) is invalid: the line along +i stops at (2,0) without measuring it
+    lat = sp.Lattice([list(range(5)), list(range(3))], predicate=lambda p: p != (3, 0))
+    calls = []
+
+    def cost(p):
+        calls.append(tuple(p))
+        return (p[0] - 4) ** 2 + 3 * p[1]
+
+    res = dr.droplet(lat, cost, start=(0, 0), line=True)
+    assert (3, 0) not in calls
+    # from (2,0) the scan goes to (2,1)... only if better; (2,1) costs 7 > 4, so it stops
+    assert res["best"] == (2, 0) and all(lat.valid(p) for p in calls)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_line_exhaustive_convex_every_start(seed):
+    rng = np.random.default_rng(seed)
+    lat = sp.Lattice([list(range(5)), list(range(4)), list(range(3))])
+    centers = rng.uniform(0, 4, size=3)
+    weights = rng.uniform(0.5, 2.0, size=3) + np.array([0.0, 1e-3, 2e-3]) * math.pi
+    cost = convex_cost(centers, weights)
+    gmin = min(lat.valid_points(), key=cost)
+    for start in lat.valid_points():
+        res = dr.droplet(lat, cost, start=start, budget=1000, line=True)
+        assert res["best"] == gmin
+
+
 @pytest.mark.parametrize("seed", range(10))
-def test_multimodal_local_optimum(seed):
+def test_line_fewer_trials_on_one_axis_descents(seed):
+    # long axes, separable convex cost, start in a corner: steps replace scans
+    rng = np.random.default_rng(300 + seed)
+    lat = sp.Lattice([list(range(12)), list(range(10)), list(range(3))])
+    cost = convex_cost(rng.uniform(8, 11, size=3) * [1, 0.9, 0.2], rng.uniform(0.5, 2.0, size=3))
+    a = dr.droplet(lat, cost, start=(0, 0, 0), budget=1000)
+    b = dr.droplet(lat, cost, start=(0, 0, 0), budget=1000, line=True)
+    assert b["best"] == a["best"] and b["measured"] < a["measured"]
+
+
+@pytest.mark.parametrize("line", [False, True])
+@pytest.mark.parametrize("seed", range(10))
+def test_multimodal_local_optimum(seed, line):
     rng = np.random.default_rng(100 + seed)
     lat = sp.Lattice([list(range(5)), list(range(4)), list(range(3))],
                      predicate=lambda p: (p[0] + 2 * p[1] + p[2]) % 7 != 3)
@@ -84,7 +158,7 @@ def test_multimodal_local_optimum(seed):
         calls.append(lat.key(idx))
         return table[tuple(idx)]
 
-    res = dr.droplet(lat, cost, budget=1000)
+    res = dr.droplet(lat, cost, budget=1000, line=line)
     best = res["best"]
     assert all(table[nb] >= table[best] for nb in lat.neighbors(best))
     assert table[best] >= min(table[p] for p in lat.valid_points())
