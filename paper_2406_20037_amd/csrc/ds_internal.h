@@ -119,7 +119,30 @@ struct MatmulArgs {
     int vecA, vecB;       // 1: 16-byte loads along K of A / along N of B are legal
     int direct;           // 1: every tile is full and aligned: K-tiles go straight to LDS
     float *part;          // ks > 1: split z writes its partial C at part + z * M*N
+    int gm;               // tile rows per group of the XCD tile order (mm_group_rows)
 };
+
+// Tile rows per group of the matmul tile order: the power of two (at most
+// tiles_m) that minimises the A rows plus B columns, in elements, touched by
+// the contiguous tile range of one XCD (ties: the smaller), so that range is
+// square in elements whatever the tile's aspect.
+inline int mm_group_rows(int tiles_m, int tiles_n, int ks, int bm, int bn) {
+    const int64_t tiles = int64_t(tiles_m) * tiles_n * ks;
+    const int64_t per_xcd = tiles > 8 ? (tiles + 7) / 8 : 1;
+    int best = 1;
+    int64_t cost = INT64_MAX;
+    for (int gm = 1; gm <= tiles_m && gm > 0; gm *= 2) {
+        const int64_t rows = gm < per_xcd ? gm : per_xcd;
+        int64_t cols = (per_xcd + gm - 1) / gm;
+        if (cols > tiles_n) cols = tiles_n;
+        const int64_t c = rows * bm + cols * bn;
+        if (c < cost) {
+            cost = c;
+            best = gm;
+        }
+    }
+    return best;
+}
 
 struct Plan {
     const void *func = nullptr;

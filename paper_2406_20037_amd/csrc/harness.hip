@@ -267,6 +267,7 @@ void fill_mm_args(const Space &sp, const float *A, const float *B, float *C, Mat
     a.M = int(sp.shape[0]);
     a.N = int(sp.shape[1]);
     a.K = int(sp.shape[2]);
+    a.gm = 1;
 }
 
 double elapsed_ms(hipEvent_t a, hipEvent_t b) {
@@ -485,6 +486,7 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.vecA = (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
         a.vecB = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
         a.direct = a.vecA && a.vecB && a.M % bm == 0 && a.N % bn == 0 && a.K % bk == 0;
+        a.gm = mm_group_rows(a.tiles_m, a.tiles_n, a.ks, bm, bn);
         plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf, kg)
                          : mm_valu_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf);
         plan.splits = a.ks > 1 ? int(cdiv64(a.nkt, a.kps)) : 1;

@@ -36,18 +36,18 @@ namespace {
 #define DS_GLOBAL(p) ((const __attribute__((address_space(1))) void *)(p))
 #define DS_LOCAL(p) ((__attribute__((address_space(3))) void *)(p))
 
-// Tiles in groups of up to kGroupM tile rows, column-major inside a group, so
-// the contiguous tile range of one XCD touches few rows of A and columns of B.
-constexpr int kGroupM = 4;
-
+// Tiles in groups of a.gm tile rows (chosen on the host: the XCD's range of
+// tiles square in elements), column-major inside a group, so the contiguous
+// tile range of one XCD touches few rows of A and columns of B.
 __device__ __forceinline__ void mm_tile_coords(const MatmulArgs &a, int &mt, int &nt, int &z) {
     const int tiles = a.tiles_m * a.tiles_n;
     const int t = xcd_tile(blockIdx.x, gridDim.x);
     z = t / tiles;
     const int r = t - z * tiles;
-    const int gsz = kGroupM * a.tiles_n;
-    const int g = r / gsz, first = g * kGroupM;
-    const int rows = min(a.tiles_m - first, kGroupM);
+    const int gm = a.gm;
+    const int gsz = gm * a.tiles_n;
+    const int g = r / gsz, first = g * gm;
+    const int rows = min(a.tiles_m - first, gm);
     const int rg = r - g * gsz;
     mt = first + rg % rows;
     nt = rg / rows;
