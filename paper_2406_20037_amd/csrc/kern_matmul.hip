@@ -53,6 +53,31 @@ __device__ __forceinline__ void mm_tile_coords(const MatmulArgs &a, int &mt, int
     nt = rg / rows;
 }
 
+// Lane exchange inside quads of lanes (DPP quad_perm).
+template <int CTRL>
+__device__ __forceinline__ float quad_perm(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// 4x4 transpose across the four lanes of a quad: lane b's x[j] becomes lane
+// j's x[b].  Two rounds of 2x2 swaps: lanes b, b^1 on register pairs (0,1),
+// (2,3), then lanes b, b^2 on pairs (0,2), (1,3).
+__device__ __forceinline__ void quad_transpose(float (&x)[4], int b) {
+    const bool o1 = b & 1, o2 = b & 2;
+#pragma unroll
+    for (int p = 0; p < 4; p += 2) {
+        const float r = quad_perm<0xB1>(o1 ? x[p] : x[p + 1]);   // lanes [1,0,3,2]
+        x[p] = o1 ? r : x[p];
+        x[p + 1] = o1 ? x[p + 1] : r;
+    }
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const float r = quad_perm<0x4E>(o2 ? x[p] : x[p + 2]);   // lanes [2,3,0,1]
+        x[p] = o2 ? r : x[p];
+        x[p + 2] = o2 ? x[p + 2] : r;
+    }
+}
+
 // Slot permutation of A row r (BK/4 slots per row).
 template <int BK>
 __device__ __forceinline__ int a_swz(int r) {
@@ -617,6 +642,33 @@ __global__ __launch_bounds__(256 * KG) void mm_mfma(MatmulArgs a) {
     // Output layout: 32x32 block, lane holds rows 8*(v/4) + 4*lg + v%4 of
     // column li (v < 16); 16x16 block, rows 4*lg + v of column li (v < 4).
     float *cbase = a.ks > 1 ? a.part + (size_t)z * a.M * a.N : a.C;
+    if constexpr (!BIG && NB % 4 == 0) {
+        // Four 16x16 blocks side by side: lane 4q+b holds columns 16j + 4q + b
+        // (j < 4) of a row; a 4x4 transpose inside each lane quad leaves it
+        // columns 16b + 4q .. +3, so every lane stores 16 contiguous bytes and
+        // a row's 64 columns go out as whole 256-byte segments (non-temporal,
+        // like the 32x32 blocks).  Full aligned tiles only.
+        if (a.direct && (reinterpret_cast<uintptr_t>(cbase) & 15) == 0) {
+            const int b = li & 3, q4 = li >> 2;
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int v = 0; v < NV; ++v) {
+                    const int gm = m0 + wr * WM + i * IM + 4 * lg + v;
+#pragma unroll
+                    for (int jq = 0; jq < NB / 4; ++jq) {
+                        float x[4] = {acc[i][4 * jq][v], acc[i][4 * jq + 1][v],
+                                      acc[i][4 * jq + 2][v], acc[i][4 * jq + 3][v]};
+                        quad_transpose(x, b);
+                        const int gn = n0 + wc * WN + jq * 64 + 16 * b + 4 * q4;
+                        __builtin_nontemporal_store(
+                            floatx4{x[0], x[1], x[2], x[3]},
+                            reinterpret_cast<floatx4 *>(cbase + (size_t)gm * a.N + gn));
+                    }
+                }
+            return;
+        }
+    }
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
