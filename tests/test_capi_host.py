@@ -252,3 +252,54 @@ def test_single_hip_runtime_in_process():
                          cwd=lib.HERE + "/..", timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_degenerate_tuning_cases():
+    """The method's degenerate cases through the C ABI and in the oracle:
+    nothing to explore, nothing valid, an exploration that exhausts the
+    lattice, a Droplet start at the origin when the origin is invalid, and a
+    zero Droplet budget."""
+    vals = [list(range(3)), list(range(4))]
+    pred = lambda p: (p[0] + p[1]) % 3 != 0          # (0, 0) is invalid
+    o = osp.Lattice(vals, predicate=pred)
+    inv = [k for k in range(o.size()) if not o.valid(o.from_key(k))]
+    c = lib.Space(lattice=vals, invalid_keys=inv)
+    cost = lambda p: float((p[0] - 2) ** 2 + (p[1] - 1) ** 2 + 0.1 * p[1])
+
+    # no exploration budget: nothing to hand to Droplet Search
+    assert odr.combined(o, cost, seed=1, n_explore=0)["status"] == odr.EEXHAUSTED
+    with pytest.raises(lib.DsError) as e:
+        lib.ds_tune(c, lib.tune_cfg(n_explore=0, seed=1), None, cost)
+    assert e.value.rc == lib.DS_EEXHAUSTED
+
+    # a lattice without a valid point
+    dead = osp.Lattice(vals, predicate=lambda p: False)
+    cd = lib.Space(lattice=vals, invalid_keys=list(range(dead.size())))
+    assert odr.combined(dead, cost, seed=1, n_explore=5)["status"] == odr.EEXHAUSTED
+    with pytest.raises(lib.DsError) as e:
+        lib.ds_tune(cd, lib.tune_cfg(n_explore=5, seed=1), None, cost)
+    assert e.value.rc == lib.DS_EEXHAUSTED
+
+    # exploring more points than the lattice holds measures every valid point
+    # once; Droplet then finds every neighbour cached and stops at the optimum
+    nvalid = len(o.valid_points())
+    ref = odr.combined(o, cost, seed=2, n_explore=50)
+    res, _ = lib.ds_tune(c, lib.tune_cfg(n_explore=50, seed=2, alpha=1.0), None, cost)
+    assert res.n_explore_measured == ref["n_explore"] == nvalid
+    assert res.best.index() == ref["best"] == min(o.valid_points(), key=cost)
+    assert res.n_droplet_measured == ref["n_droplet"] == 0
+
+    # Droplet from "no optimisation": the origin is invalid, so the first
+    # valid point in key order
+    ref = odr.droplet(o, cost, start=None, budget=100)
+    res, trace = lib.droplet_tune_ex(c, None, 100, lib.tune_cfg(alpha=1.0), None, cost,
+                                     trace_cap=64)
+    assert ref["path"][0] == o.origin() == (1, 0)
+    assert res.seed_point.index() == (1, 0)
+    assert res.best.index() == ref["best"] and [t[2] for t in trace] == ref["order"]
+
+    # a zero budget measures the start only
+    ref = odr.droplet(o, cost, start=(1, 0), budget=0)
+    res, _ = lib.droplet_tune_ex(c, (1, 0), 0, lib.tune_cfg(alpha=1.0), None, cost)
+    assert ref["status"] == odr.EBUDGET and res.status == lib.DS_EBUDGET
+    assert res.n_droplet_measured == ref["measured"] == 1 and res.best.index() == (1, 0)
