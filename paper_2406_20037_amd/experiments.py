@@ -5,6 +5,7 @@ with line steps, Random, Grid and GA), the exploration-budget sweep
 object per result line on stdout and progress on stderr.
 
     python -m paper_2406_20037_amd.experiments exploiters --workload matmul_1024 --seeds 3
+    python -m paper_2406_20037_amd.experiments exploiters --workload vgg16:L6_256_256_56
     python -m paper_2406_20037_amd.experiments sweep --workload conv3x3_c64_56 --seeds 3
     python -m paper_2406_20037_amd.experiments tasks --workload resnet50 --trials 24,300,1000
     python -m paper_2406_20037_amd.experiments report out/*.jsonl
@@ -66,16 +67,24 @@ class Task:
 
 
 def single_task(L, workload, stream):
+    """A single kernel or one layer of a network ("vgg16:L6_256_256_56");
+    returns the task and the base seed of its exploration stream."""
     from synthdata import workloads as wl
+    if ":" in workload:
+        net, layer = workload.split(":", 1)
+        layers, config = {"resnet50": (wl.RESNET50, 3), "vgg16": (wl.VGG16, 4)}[net]
+        j = next(i for i, (n, _, _, _) in enumerate(layers) if n == layer)
+        _, op, shape, _ = layers[j]
+        return Task(L, workload, op, shape, "he", stream), wl.sampler_seed(config, j)
     op, shape = wl.SINGLE[workload]
-    return Task(L, workload, op, shape, "uniform", stream), CONFIG_OF[workload]
+    return Task(L, workload, op, shape, "uniform", stream), wl.sampler_seed(CONFIG_OF[workload])
 
 
 def run_exploiters(L, args, stream):
     from synthdata import workloads as wl
-    task, config = single_task(L, args.workload, stream)
+    task, base_seed = single_task(L, args.workload, stream)
     for s in range(args.seeds):
-        seed = wl.sampler_seed(config) + s
+        seed = base_seed + s
         cache = L.Cache(task.space)
         ex, _ = L.ds_explore(task.space, cache, L.tune_cfg(n_explore=args.n_explore, seed=seed),
                              task.io)
@@ -106,10 +115,10 @@ def run_exploiters(L, args, stream):
 
 def run_sweep(L, args, stream):
     from synthdata import workloads as wl
-    task, config = single_task(L, args.workload, stream)
+    task, base_seed = single_task(L, args.workload, stream)
     ns = [int(v) for v in args.ns.split(",")]
     for s in range(args.seeds):
-        seed = wl.sampler_seed(config) + s
+        seed = base_seed + s
         for n in ns:
             res, _ = L.ds_tune(task.space, L.tune_cfg(n_explore=n, budget=args.budget, seed=seed),
                                task.io)
@@ -126,7 +135,7 @@ def run_sweep(L, args, stream):
             emit(row)
     if args.random_10k:
         cache = L.Cache(task.space)
-        seed = wl.sampler_seed(config) + 999
+        seed = base_seed + 999
         ex, _ = L.ds_explore(task.space, cache, L.tune_cfg(n_explore=10000, seed=seed), task.io)
         best_us = task.retime_us(ex.seed_point)
         row = dict(experiment="sweep", workload=args.workload, seed=seed, n_explore=10000,
