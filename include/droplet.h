@@ -373,7 +373,9 @@ void ds_exploit_cfg_default(ds_exploit_cfg *cfg);
  * candidates without charge, stop after cfg->budget charged trials or when
  * their candidate stream ends (Random: 100*budget draws; Grid: back at the
  * start; GA: neither crossover nor the Random stream yields a new point), and
- * return the fastest of the start and their trials (ties: earliest).
+ * return the fastest of the start and their trials (ties: earliest).  Droplet
+ * and Droplet with line steps run as droplet_tune_ex with cfg->budget (they
+ * visit valid points only, so valid_only has no effect on them).
  * tcfg supplies alpha, frozen_mask (Droplet) and the measurement settings.
  * cache may be NULL (a private one is used).  res->n_droplet_measured counts
  * the strategy's measurements (start included when measured), res->n_failed
