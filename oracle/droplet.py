@@ -26,7 +26,11 @@ Readings taken where the paper is silent or loose:
   neighbour measurements; the start point, when not already measured, is
   measured once more and reported in ``measured`` but not charged to the
   budget.  Measured points are cached and never measured twice; a failed
-  measurement has infinite time and still counts.
+  measurement has infinite time and still counts.  When the budget runs out
+  part-way through a neighbourhood, the neighbours already measured in it are
+  still compared with the current point (and the move taken if one is
+  faster) before the search stops: the paper's stopping rule is the trial
+  count, and a trial that was run is part of the search.
 * ``frozen`` lists axes that are held at the start's value (the single-sketch
   variant of Section 2.2's first limitation).
 * ``line`` (not the method of the paper's experiments): Section 2.2 presents
@@ -160,12 +164,17 @@ def droplet(space, cost, start=None, budget=100, alpha=1.0, cache=None, frozen=(
             cache[kn] = Meas.of(cost(nb))
             nb_measured += 1
             order.append(kn)
-        if stop or not nbs:
-            break
+        # The fastest neighbour among those measured (ties: first in neighbour
+        # order).  A budget stop part-way through the neighbourhood still lets
+        # the neighbours measured before it compete: their trials were spent.
         best_nb = None
         for nb in nbs:
+            if space.key(nb) not in cache:
+                continue
             if best_nb is None or cache[space.key(nb)].median < cache[space.key(best_nb)].median:
                 best_nb = nb
+        if best_nb is None:
+            break
         if not better(cache[space.key(best_nb)], cache[space.key(cur)], alpha):
             break
         axis = next(a for a in range(len(cur)) if best_nb[a] != cur[a])

@@ -175,16 +175,22 @@ DropletOut droplet(const Space &sp, const int32_t *start, int budget, double alp
             out.measured++;
             trace_push(trace, 2, m, k);
         }
-        if (stop || nbs.empty()) break;
-        size_t b = 0;
-        for (size_t i = 1; i < nbs.size(); ++i)
-            if (cache[sp.key(nbs[i].data())].median < cache[sp.key(nbs[b].data())].median) b = i;
-        const Meas &mb = cache[sp.key(nbs[b].data())];
+        // The fastest measured neighbour (ties: first in neighbour order).  When
+        // the budget ran out part-way through the neighbourhood, the neighbours
+        // measured before it did still compete: they were paid for.
+        int b = -1;
+        for (size_t i = 0; i < nbs.size(); ++i) {
+            auto it = cache.find(sp.key(nbs[i].data()));
+            if (it == cache.end()) continue;
+            if (b < 0 || it->second.median < cache[sp.key(nbs[size_t(b)].data())].median) b = int(i);
+        }
+        if (b < 0) break;
+        const Meas &mb = cache[sp.key(nbs[size_t(b)].data())];
         if (!better(mb, cache[kcur], alpha)) break;
         int axis = 0;
-        while (nbs[b][axis] == cur[axis]) ++axis;
-        const int dir = nbs[b][axis] - cur[axis];
-        cur = nbs[b];
+        while (nbs[size_t(b)][axis] == cur[axis]) ++axis;
+        const int dir = nbs[size_t(b)][axis] - cur[axis];
+        cur = nbs[size_t(b)];
         kcur = sp.key(cur.data());
         out.moves++;
         while (line) {

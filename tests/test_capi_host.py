@@ -200,6 +200,24 @@ def test_budget_and_failures_through_c_abi():
     assert res.best.index() == ref["best"] and [t[2] for t in trace] == ref["order"]
 
 
+def test_budget_stop_mid_neighbourhood_through_c_abi():
+    """The budget runs out inside a neighbourhood after a faster neighbour was
+    measured: the search still moves there (the hand-worked case of the
+    oracle's budget pin on Example 3's lattice)."""
+    vals = [[1, 2, 3, 4, 5], [1, 2, 4, 8, 16]]
+    c = lib.Space(lattice=vals)
+    o = osp.Lattice(vals)
+    cost = lambda p: float((vals[0][p[0]] - 4) ** 2 + (math.log2(vals[1][p[1]]) - 1) ** 2)
+    for budget, best in ((2, (1, 0)), (3, (2, 0))):
+        res, trace = lib.droplet_tune_ex(c, (0, 0), budget, lib.tune_cfg(alpha=1.0), None, cost,
+                                         trace_cap=16)
+        ref = odr.droplet(o, cost, start=(0, 0), budget=budget)
+        assert res.status == lib.DS_EBUDGET and ref["status"] == odr.EBUDGET
+        assert res.best.index() == ref["best"] == best
+        assert [t[2] for t in trace] == ref["order"]
+        assert res.best_ms == ref["meas"].median
+
+
 def test_frozen_axes_through_c_abi():
     vals = [list(range(4)), [0, 1]]
     c = lib.Space(lattice=vals)

@@ -45,10 +45,19 @@ def test_hand_trace(golden_dir):
 
 
 def test_budget_stops_and_counts():
+    # Worked by hand on Example 3's lattice, cost (u-4)^2 + (log2 t - 1)^2 from
+    # (u,t) = (1,1) (cost 10), budget 3.  Scan 1: (2,1) = 5 and (1,2) = 9, two
+    # trials; move to (2,1).  Scan 2: (1,1) is cached, (3,1) = 2 is the third
+    # trial, (2,2) would be the fourth: the budget stops the scan there, but
+    # (3,1) was measured and beats (2,1), so the search ends on it.
     lat = example3_lattice()
     res = dr.droplet(lat, example3_cost(lat), budget=3)
     assert res["status"] == dr.EBUDGET and res["measured"] == 4
-    assert [tuple(p) for p in res["path"]] == [(0, 0), (1, 0)]
+    assert [tuple(p) for p in res["path"]] == [(0, 0), (1, 0), (2, 0)]
+    assert res["best"] == (2, 0) and res["meas"].median == 2.0
+    # budget 2: scan 2 stops before (3,1), nothing measured there beats (2,1)
+    res2 = dr.droplet(lat, example3_cost(lat), budget=2)
+    assert res2["status"] == dr.EBUDGET and res2["best"] == (1, 0) and res2["measured"] == 3
     res0 = dr.droplet(lat, example3_cost(lat), budget=0)
     assert res0["status"] == dr.EBUDGET and res0["measured"] == 1 and res0["best"] == (0, 0)
 
