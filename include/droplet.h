@@ -160,7 +160,16 @@ int sched_has_kernel(const ds_space *space, const ds_sched *s);
  * w[k,c,r,s], out-of-range inputs read as 0.  matmul: x = A [M,K], w = B
  * [K,N], y = C [M,N] = A*B, row-major.  fp32 in, out and accumulate.
  * Asynchronous on stream; y is overwritten.  An empty output launches nothing.
- * Errors: DS_EINVAL, DS_EINVALID_SCHED (nothing launched), DS_EHIP.
+ * A split reduction (ks > 1) writes its partial outputs to a workspace the
+ * library keeps per (device, stream): split launches on different streams do
+ * not share partials.  When a stream's workspace is too small it is replaced
+ * by a larger one (hipMalloc; the old one is kept until ds_shutdown, since a
+ * graph captured earlier may still use it, and the stream is synchronised
+ * first).  Under stream capture nothing may be allocated: a split schedule
+ * whose workspace does not exist yet on that stream returns DS_EUNSUPPORTED
+ * (run it once on the stream before capturing).
+ * Errors: DS_EINVAL, DS_EINVALID_SCHED (nothing launched), DS_EHIP,
+ * DS_ENOMEM, DS_EUNSUPPORTED.
  */
 int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float *y,
                hipStream_t stream);

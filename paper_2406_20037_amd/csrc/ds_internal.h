@@ -159,7 +159,7 @@ struct Plan {
 // Builds the plan of schedule s for buffers (x, w, y); DS_EINVALID_SCHED if s is
 // not a valid point.
 int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan &plan);
-int attach_workspace(Plan &plan);     // split reductions: library-owned partial buffer
+int attach_workspace(Plan &plan, hipStream_t stream);   // split reductions: per-stream partials
 int launch_plan(const Plan &plan, hipStream_t stream);
 
 // Kernel instance lookup (compiled template instances).

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstring>
 #include <limits>
+#include <map>
 #include <mutex>
 #include <set>
 #include <utility>
@@ -160,8 +161,16 @@ constexpr int kMaxDevices = 64;
 std::mutex g_mu;
 unsigned *g_parity_buf[kMaxDevices];     // 4 words per device, library-owned
 hipStream_t g_graph_stream[kMaxDevices];  // capture / replay stream per device
-float *g_split_ws[kMaxDevices];           // partial outputs of split reductions
-int64_t g_split_ws_elems[kMaxDevices];
+// Partial outputs of split reductions: one buffer per (device, stream), so
+// split launches on different streams never share partials.  A buffer that
+// grows is retired, not freed: a graph the caller captured earlier may still
+// hold its address.  Retired and live buffers are freed by ds_shutdown.
+struct SplitWs {
+    float *p = nullptr;
+    int64_t elems = 0;
+};
+std::map<std::pair<int, hipStream_t>, SplitWs> g_split_ws;
+std::vector<std::pair<int, void *>> g_split_retired;
 std::set<std::pair<int, const void *>> g_lds_attr;
 
 int current_device(int &dev) {
@@ -202,28 +211,42 @@ int graph_stream(hipStream_t *out) {
     return DS_OK;
 }
 
-// The per-device workspace of split reductions, grown to at least `elems`
-// floats (kernels queued earlier on any stream must not still be using it:
-// split-reduction launches on one device are expected to be stream-ordered).
-int split_workspace(int64_t elems, float **out) {
+// The split-reduction workspace of `stream` on the current device, grown to at
+// least `elems` floats.  Growing allocates a new buffer (at least twice the
+// old size) and retires the old one after the stream's queued work is done;
+// while the stream is being captured nothing may be allocated, so a capture
+// needs the buffer to exist already (one uncaptured call of the same schedule
+// on that stream creates it).
+int split_workspace(int64_t elems, hipStream_t stream, float **out) {
     int dev;
     int rc = current_device(dev);
     if (rc != DS_OK) return rc;
     std::lock_guard<std::mutex> lk(g_mu);
-    if (g_split_ws_elems[dev] < elems) {
-        if (g_split_ws[dev]) {
-            if (!hip_ok(hipDeviceSynchronize(), "hipDeviceSynchronize")) return DS_EHIP;
-            (void)hipFree(g_split_ws[dev]);
-            g_split_ws[dev] = nullptr;
-            g_split_ws_elems[dev] = 0;
+    SplitWs &ws = g_split_ws[{dev, stream}];
+    if (ws.elems < elems) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (!hip_ok(hipStreamIsCapturing(stream, &cap), "hipStreamIsCapturing")) return DS_EHIP;
+        if (cap != hipStreamCaptureStatusNone) {
+            set_error("split reduction needs %lld workspace floats on a stream under capture; run "
+                      "the schedule once on that stream outside capture first",
+                      (long long)elems);
+            return DS_EUNSUPPORTED;
         }
+        const int64_t grow = std::max<int64_t>(elems, 2 * ws.elems);
         void *p = nullptr;
-        if (!hip_ok(hipMalloc(&p, size_t(elems) * sizeof(float)), "hipMalloc(split workspace)"))
+        if (!hip_ok(hipMalloc(&p, size_t(grow) * sizeof(float)), "hipMalloc(split workspace)"))
             return DS_ENOMEM;
-        g_split_ws[dev] = static_cast<float *>(p);
-        g_split_ws_elems[dev] = elems;
+        if (ws.p) {
+            if (!hip_ok(hipStreamSynchronize(stream), "hipStreamSynchronize")) {
+                (void)hipFree(p);
+                return DS_EHIP;
+            }
+            g_split_retired.emplace_back(dev, ws.p);
+        }
+        ws.p = static_cast<float *>(p);
+        ws.elems = grow;
     }
-    *out = g_split_ws[dev];
+    *out = ws.p;
     return DS_OK;
 }
 
@@ -499,16 +522,26 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
     return DS_OK;
 }
 
-int attach_workspace(Plan &plan) {
-    if (plan.splits <= 1 || plan.y_elems == 0 || plan.grid == 0) return DS_OK;
+int64_t workspace_elems(const Plan &plan) {
+    if (plan.splits <= 1 || plan.y_elems == 0 || plan.grid == 0) return 0;
     // Splits that own no reduction step exit early; the reduce kernel sums only
     // the first plan.splits partial slices.
-    float *part = nullptr;
     const int ks = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.ks : plan.mm.ks;
-    const int rc = split_workspace(int64_t(ks) * plan.y_elems, &part);
-    if (rc != DS_OK) return rc;
+    return int64_t(ks) * plan.y_elems;
+}
+
+void set_workspace(Plan &plan, float *part) {
     if (plan.op == DS_OP_CONV2D_NCHW) plan.conv.part = part;
     else plan.mm.part = part;
+}
+
+int attach_workspace(Plan &plan, hipStream_t stream) {
+    const int64_t elems = workspace_elems(plan);
+    if (elems == 0) return DS_OK;
+    float *part = nullptr;
+    const int rc = split_workspace(elems, stream, &part);
+    if (rc != DS_OK) return rc;
+    set_workspace(plan, part);
     return DS_OK;
 }
 
@@ -604,7 +637,7 @@ int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float 
         set_error("null buffer");
         return DS_EINVAL;
     }
-    rc = attach_workspace(plan);
+    rc = attach_workspace(plan, stream);
     if (rc != DS_OK) return rc;
     return launch_plan(plan, stream);
 }
@@ -702,7 +735,7 @@ int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cf
         set_error("null buffer");
         return DS_EINVAL;
     }
-    rc = attach_workspace(plan);
+    rc = attach_workspace(plan, io->stream);
     if (rc != DS_OK) {
         out->status = rc;
         return DS_OK;
@@ -883,18 +916,24 @@ void ds_shutdown(void) {
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return;
     for (int d = 0; d < kMaxDevices; ++d) {
-        if (!g_parity_buf[d] && !g_graph_stream[d] && !g_split_ws[d]) continue;
+        bool ws = false;
+        for (auto &e : g_split_ws) ws = ws || e.first.first == d;
+        for (auto &e : g_split_retired) ws = ws || e.first == d;
+        if (!g_parity_buf[d] && !g_graph_stream[d] && !ws) continue;
         if (hipSetDevice(d) == hipSuccess) {
             (void)hipDeviceSynchronize();
             if (g_parity_buf[d]) (void)hipFree(g_parity_buf[d]);
             if (g_graph_stream[d]) (void)hipStreamDestroy(g_graph_stream[d]);
-            if (g_split_ws[d]) (void)hipFree(g_split_ws[d]);
+            for (auto &e : g_split_ws)
+                if (e.first.first == d && e.second.p) (void)hipFree(e.second.p);
+            for (auto &e : g_split_retired)
+                if (e.first == d) (void)hipFree(e.second);
         }
         g_parity_buf[d] = nullptr;
         g_graph_stream[d] = nullptr;
-        g_split_ws[d] = nullptr;
-        g_split_ws_elems[d] = 0;
     }
+    g_split_ws.clear();
+    g_split_retired.clear();
     (void)hipSetDevice(cur);
     g_lds_attr.clear();
 }

@@ -859,7 +859,7 @@ int ds_exploit(const ds_space *space, const ds_sched *start, const ds_exploit_cf
             c.emplace(k0, std::move(m));
             start_measured = 1;
         }
-        ExploitRun run{sp, c, measure, cfg.budget, cfg.valid_only != 0, best_so_far, trace};
+        ExploitRun run{sp, c, measure, cfg.budget, cfg.valid_only != 0, best_so_far, trace, 0, 0, {}};
         if (cfg.kind == DS_EXPLOIT_RANDOM) {
             SplitMix64 rng(cfg.seed);
             RandomStream rs{rng, 100 * int64_t(cfg.budget)};
