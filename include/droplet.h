@@ -167,12 +167,31 @@ int sched_has_kernel(const ds_space *space, const ds_sched *s);
  * graph captured earlier may still use it, and the stream is synchronised
  * first).  Under stream capture nothing may be allocated: a split schedule
  * whose workspace does not exist yet on that stream returns DS_EUNSUPPORTED
- * (run it once on the stream before capturing).
+ * (run it once on the stream before capturing, or use kernel_run_noalloc).
  * Errors: DS_EINVAL, DS_EINVALID_SCHED (nothing launched), DS_EHIP,
  * DS_ENOMEM, DS_EUNSUPPORTED.
  */
 int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float *y,
                hipStream_t stream);
+
+/*
+ * kernel_run_noalloc -- kernel_run for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  It launches the same kernels as kernel_run, but the
+ * partial outputs of a split reduction (ks > 1) go to a fixed array in device
+ * memory (one per device, DS_NOALLOC_MAX_FLOATS floats = 32 MiB, held by the
+ * library until the process ends) instead of a library-allocated workspace.
+ * It calls no hipMalloc or hipFree.  A split schedule whose partials (ks *
+ * output elements) exceed DS_NOALLOC_MAX_FLOATS floats is rejected with
+ * DS_EINVAL and launches nothing.  Every call on one device shares that device's array:
+ * calls that overlap in time on one device (different streams, or different
+ * host threads) race on it and give wrong outputs; order them on one stream.
+ * The array is fully rewritten by each split launch before it is read, so it
+ * needs no clearing.  Arguments, layout and other errors as kernel_run.
+ */
+#define DS_NOALLOC_MAX_FLOATS 8388608
+int kernel_run_noalloc(int op, const ds_sched *s, const float *x, const float *w, float *y,
+                       hipStream_t stream);
 
 /* The library's plain one-thread-per-output kernel for the same operation
  * (used as the in-tuning reference when the caller supplies none). */

@@ -42,6 +42,7 @@ DS_OP_CONV2D_NCHW = 1
 DS_OP_MATMUL_RM = 2
 DS_MAX_KNOBS = 12
 DS_MAX_REPEATS = 64
+DS_NOALLOC_MAX_FLOATS = 8388608   # kernel_run_noalloc: split partials capacity
 
 
 class ds_sched(C.Structure):
@@ -145,6 +146,8 @@ SIGNATURES = {
     "sched_has_kernel": (C.c_int, [C.c_void_p, C.POINTER(ds_sched)]),
     "kernel_run": (C.c_int, [C.c_int, C.POINTER(ds_sched), C.c_void_p, C.c_void_p, C.c_void_p,
                              C.c_void_p]),
+    "kernel_run_noalloc": (C.c_int, [C.c_int, C.POINTER(ds_sched), C.c_void_p, C.c_void_p,
+                                     C.c_void_p, C.c_void_p]),
     "kernel_run_reference": (C.c_int, [C.c_int, C.POINTER(C.c_int64), C.c_void_p, C.c_void_p,
                                        C.c_void_p, C.c_void_p]),
     "ds_measure_cfg_default": (None, [C.POINTER(ds_measure_cfg)]),
@@ -359,6 +362,12 @@ class Space:
 def kernel_run(op, sched, x, w, y, stream=None):
     return check("kernel_run", lib.kernel_run(op, C.byref(sched), ptr(x), ptr(w), ptr(y),
                                               stream_handle(stream)))
+
+
+def kernel_run_noalloc(op, sched, x, w, y, stream=None):
+    return check("kernel_run_noalloc",
+                 lib.kernel_run_noalloc(op, C.byref(sched), ptr(x), ptr(w), ptr(y),
+                                        stream_handle(stream)))
 
 
 def kernel_run_reference(op, shape, x, w, y, stream=None):

@@ -173,6 +173,14 @@ std::map<std::pair<int, hipStream_t>, SplitWs> g_split_ws;
 std::vector<std::pair<int, void *>> g_split_retired;
 std::set<std::pair<int, const void *>> g_lds_attr;
 
+// Split-reduction partials of kernel_run_noalloc: a fixed array in device
+// memory (one copy per device, held until the process ends), so that entry
+// point never allocates.  Host code never passes the array's name to a kernel:
+// g_scratch[dev] holds the address the runtime reports for this device.
+constexpr int64_t kScratchFloats = DS_NOALLOC_MAX_FLOATS;   // 32 MiB
+static __device__ __align__(256) float scratch[kScratchFloats];
+float *g_scratch[kMaxDevices];
+
 int current_device(int &dev) {
     if (!hip_ok(hipGetDevice(&dev), "hipGetDevice")) return DS_EHIP;
     if (dev < 0 || dev >= kMaxDevices) {
@@ -228,7 +236,8 @@ int split_workspace(int64_t elems, hipStream_t stream, float **out) {
         if (!hip_ok(hipStreamIsCapturing(stream, &cap), "hipStreamIsCapturing")) return DS_EHIP;
         if (cap != hipStreamCaptureStatusNone) {
             set_error("split reduction needs %lld workspace floats on a stream under capture; run "
-                      "the schedule once on that stream outside capture first",
+                      "the schedule once on that stream outside capture first, or use "
+                      "kernel_run_noalloc",
                       (long long)elems);
             return DS_EUNSUPPORTED;
         }
@@ -247,6 +256,27 @@ int split_workspace(int64_t elems, hipStream_t stream, float **out) {
         ws.elems = grow;
     }
     *out = ws.p;
+    return DS_OK;
+}
+
+// This device's address of `scratch`, looked up on the first call on the
+// device (with that device current) and kept.
+int scratch_ptr(float **out) {
+    int dev;
+    int rc = current_device(dev);
+    if (rc != DS_OK) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (!hip_ok(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"))
+            return DS_EHIP;
+        if (!p) {
+            set_error("hipGetSymbolAddress(scratch) returned a null address");
+            return DS_EHIP;
+        }
+        g_scratch[dev] = static_cast<float *>(p);
+    }
+    *out = g_scratch[dev];
     return DS_OK;
 }
 
@@ -639,6 +669,35 @@ int kernel_run(int op, const ds_sched *s, const float *x, const float *w, float 
     }
     rc = attach_workspace(plan, stream);
     if (rc != DS_OK) return rc;
+    return launch_plan(plan, stream);
+}
+
+int kernel_run_noalloc(int op, const ds_sched *s, const float *x, const float *w, float *y,
+                       hipStream_t stream) {
+    if (!s || s->op != op) {
+        set_error("schedule missing or for another op");
+        return DS_EINVAL;
+    }
+    Plan plan;
+    int rc = make_plan(s, x, w, y, plan);
+    if (rc != DS_OK) return rc;
+    if (plan.y_elems > 0 && plan.grid > 0 && (!x || !w || !y)) {
+        set_error("null buffer");
+        return DS_EINVAL;
+    }
+    const int64_t elems = workspace_elems(plan);
+    if (elems > kScratchFloats) {
+        set_error("kernel_run_noalloc: the split reduction needs %lld partial floats, more than the "
+                  "%lld of its fixed scratch; use a schedule with fewer splits or kernel_run",
+                  (long long)elems, (long long)kScratchFloats);
+        return DS_EINVAL;
+    }
+    if (elems > 0) {
+        float *p = nullptr;
+        rc = scratch_ptr(&p);
+        if (rc != DS_OK) return rc;
+        set_workspace(plan, p);
+    }
     return launch_plan(plan, stream);
 }
 
