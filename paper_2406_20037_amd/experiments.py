@@ -129,6 +129,7 @@ def run_sweep(L, args, stream):
                        seed_us=round(res.seed_ms * 1e3, 3), best_us=round(best_us, 3),
                        gflops=round(task.flops / (best_us * 1e-6) / 1e9, 1),
                        explore_s=round(res.explore_s, 3), droplet_s=round(res.droplet_s, 3),
+                       seed_schedule=task.space.knobs(res.seed_point),
                        best_schedule=task.space.knobs(res.best))
             log(f"seed {seed} N={n}: droplet {res.n_droplet_measured} trials, {best_us:.2f} us, "
                 f"{res.wall_s:.1f} s")
