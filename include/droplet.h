@@ -150,6 +150,48 @@ int ansor_draw(const ds_space *space, uint64_t seed, int n_explore, ds_sched *ou
  * (host only, launches nothing). */
 int sched_has_kernel(const ds_space *space, const ds_sched *s);
 
+/* Kernel families (the sketches whose annotations the spaces enumerate). */
+enum {
+    DS_KERNEL_CONV_VALU = 1,  /* conv_valu<KPT, PPT, UF, LDS> */
+    DS_KERNEL_CONV_MFMA = 2,  /* conv_mfma<TKB, NPB, UF, LDS> */
+    DS_KERNEL_MM_VALU = 3,    /* mm_valu<RM, RN, BK, UF, DB> */
+    DS_KERNEL_MM_MFMA = 4     /* mm_mfma<WM, WN, BK, UF, DB, KG> */
+};
+
+/* The compiled program a valid schedule selects (Definition 1: an annotated
+ * sketch is a concrete program): its template instance, its launch geometry
+ * and a hash of its kernel-argument block (buffer pointers left null), so two
+ * schedules launch identical work iff instance and args_hash agree.  With
+ * with_attrs = 1 the instance's compiled attributes are read with
+ * hipFuncGetAttributes (needs a device); with 0 no HIP call is made. */
+typedef struct {
+    int32_t family;                /* DS_KERNEL_* */
+    int32_t nparams;
+    int32_t params[6];             /* template parameters in declaration order */
+    int32_t instance;              /* family * 4096 + slot in the family's table */
+    int32_t threads;               /* workgroup size */
+    int64_t grid;                  /* workgroups */
+    int32_t lds_bytes;             /* dynamic LDS per workgroup */
+    int32_t splits;                /* reduction splits across workgroups (> 1: reduce launch) */
+    uint64_t args_hash;
+    int32_t num_regs;              /* with_attrs: registers per lane */
+    int32_t max_threads_per_block; /* with_attrs: the instance's launch bound */
+    int64_t local_bytes;           /* with_attrs: scratch per lane (register spills) */
+    int64_t static_lds_bytes;      /* with_attrs: statically declared LDS */
+} ds_kernel_info;
+
+/* Errors: DS_EINVAL, DS_EINVALID_SCHED (s not valid), DS_EUNSUPPORTED (no
+ * compiled instance), DS_EHIP (attribute query failed). */
+int sched_kernel_info(const ds_space *space, const ds_sched *s, int with_attrs,
+                      ds_kernel_info *out);
+
+/* Every valid point of a kernel space in key order with the program it
+ * selects: keys[i], instances[i] and args_hashes[i] as sched_kernel_info
+ * reports them (host only, no HIP call).  Writes min(n, cap) entries; *n_out
+ * = n, the number of valid points.  For tests and tools. */
+int sched_space_programs(const ds_space *space, uint64_t *keys, int32_t *instances,
+                         uint64_t *args_hashes, int64_t cap, int64_t *n_out);
+
 /* ---- kernels ------------------------------------------------------------ */
 
 /*

@@ -19,23 +19,39 @@ conv2d (op 1), shape (N, C, H, W, K, R, S, stride, pad), axes in order
     unroll in {0, 16, 64, 512}: maximum unrolled steps of the reduction loop;
     lds in {0, 1}: stage input and weight tiles in LDS;
     ks in {1, 2, 4, 8}: reduction split over C across workgroups (kept if <= C);
-    mfma in {0, 1}: contract on fp32 MFMA (implicit GEMM) instead of VALU FMA.
+    mfma in {0, 1}: contract on fp32 MFMA (implicit GEMM) instead of VALU FMA;
+    vec in {1, 4}: floats per lane of the global -> LDS copies (4 or 16 bytes).
 
 matmul (op 2), shape (M, N, K), axes in order
     bm, bn in {16, 32, 64, 128, 256}: workgroup tile, kept if <= M, N;
     bk in {4, 8, 16, 32, 64}: K-step of one LDS stage, kept if <= K;
     unroll in {0, 16, 64, 512};  dbuf in {0, 1}: LDS double buffer;
-    mfma in {0, 1};  ks in {1, 2, 4, 8}: split-K across workgroups (kept if <= K).
+    mfma in {0, 1};  ks in {1, 2, 4, 8}: split-K across workgroups (kept if <= K);
+    vec in {1, 4}: floats per lane of the operand loads (4 or 16 bytes).
 
 Validity is the hardware and register budget of the kernel family: at most
 1024 threads and 163840 bytes of LDS per workgroup, an accumulator budget per
-lane, MFMA tile minima, a VALU conv tile of at least one wave (64 outputs, or
-the largest tile of a smaller shape), at most 2**31 - 1 workgroups, and a split no finer than the number of reduction
-steps.
+lane, register budgets of the operand rings and unrolled loops (the limits at
+which the compiled instances start to spill), MFMA tile minima, a VALU conv
+tile of at least one wave (64 outputs, or the largest tile of a smaller
+shape), at most 2**31 - 1 workgroups, a split no finer than the number of
+reduction steps, and for vec = 4 an operand that can move 16 bytes per lane.
+
+The unroll knob is TVM's auto_unroll_max_step reading: the VALU loops and the
+matmul unroll their reduction loop by the largest power of two <= unroll /
+(accumulator updates per step) (capped at 16 for conv, at the trip count for
+matmul); the MFMA conv turns that factor u into the read-ahead depth D of its
+16-step group loop (D = 3 from u = 16, 2 from u = 4, else 1).  Unroll values
+that give the same factor select the same compiled program (the saturation of
+auto_unroll_max_step).
 
 Pins: the neighbourhood reproduces Example 3 of Section 2.2
 (tests/golden/droplet_example3.txt); value lists, counts and hand-computed
-geometry of named points are checked in tests/test_oracle_space.py.
+geometry of named points are checked in tests/test_oracle_space.py.  The
+validity half (register, LDS and thread budgets) is pinned against the
+compiled kernels on the GPU (tests/test_gpu_instances.py): every instance a
+valid point of the five workloads can select launches bit-exact, spills
+nothing, and fits its launch bound and LDS.
 """
 from __future__ import annotations
 
@@ -54,8 +70,10 @@ SPLITK = [1, 2, 4, 8]
 MM_TILE = [16, 32, 64, 128, 256]
 MM_BK = [4, 8, 16, 32, 64]
 
-CONV_AXES = ["tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma"]
-MM_AXES = ["bm", "bn", "bk", "unroll", "dbuf", "mfma", "ks"]
+VEC = [1, 4]
+
+CONV_AXES = ["tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma", "vec"]
+MM_AXES = ["bm", "bn", "bk", "unroll", "dbuf", "mfma", "ks", "vec"]
 
 
 def _clip(values, extent):
@@ -183,14 +201,14 @@ class Space(Lattice):
             P, Q = conv_out(shape)
             values = [
                 _clip(POW2_64, K), _clip(POW2_64, P), _clip(POW2_64, Q), _clip(POW2_64, C),
-                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1],
+                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1], list(VEC),
             ]
             names = CONV_AXES
         else:
             M, N, K = shape
             values = [
                 _clip(MM_TILE, M), _clip(MM_TILE, N), _clip(MM_BK, K),
-                list(UNROLL), [0, 1], [0, 1], _clip(SPLITK, K),
+                list(UNROLL), [0, 1], [0, 1], _clip(SPLITK, K), list(VEC),
             ]
             names = MM_AXES
         super().__init__(values, names, predicate=lambda idx: self.geometry(idx)["valid"])
@@ -244,7 +262,9 @@ def conv_geometry(shape, v):
     # aligned halo layout (image rows of whole 16-byte groups, tiles of at
     # least 16 input columns): rows start at the 16-byte boundary at or before
     # the tile's first column, up to 3 more columns, rounded to 4
-    if W % 4 == 0 and tw * st >= 16:
+    # (only with 16-byte copies, vec = 4)
+    halo16 = v["vec"] == 4 and W % 4 == 0 and tw * st >= 16
+    if halo16:
         ws = _cdiv((tw - 1) * st + S + 3, 4) * 4
     else:
         ws = (tw - 1) * st + S
@@ -259,6 +279,22 @@ def conv_geometry(shape, v):
         lds = 8 * red
     grid = N * v["ks"] * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)
     uf = 1 if v["unroll"] == 0 else min(16, _pow2floor(max(1, v["unroll"] // body)))
+    if v["mfma"]:
+        # The MFMA family's unroll is its read-ahead depth D: 3 from 16, 2 from
+        # 4, else 1; D+1 operand sets of 4 (tkb + npb) floats must fit 96
+        # registers (192 when D = 1), the budget of its compiled instances.
+        uf = 3 if uf >= 16 else (2 if uf >= 4 else 1)
+        ring = (uf + 1) * 4 * (t0 + t1)
+        ok = ok and (ring <= 96 or (uf == 1 and ring <= 192))
+    else:
+        # 64 accumulators on the global path do not fit an unroll of 8 or more
+        ok = ok and not (v["lds"] == 0 and acc == 64 and uf >= 8)
+    # vec = 4 (16-byte copies into LDS) needs staging by whole waves and one
+    # operand whose staged rows are whole 16-byte groups
+    if v["vec"] == 4:
+        w16 = (C * R * S) % 4 == 0 and (tc * R * S) % 4 == 0 and wrow % 4 == 0
+        h16 = halo16 and (tk * wrow) % 4 == 0
+        ok = ok and v["lds"] == 1 and threads % 64 == 0 and (w16 or h16)
     valid = (ok and lds <= LDS_LIMIT and threads <= THREADS_LIMIT and v["ks"] <= chunks
              and grid <= GRID_LIMIT)
     return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=acc,
@@ -304,6 +340,18 @@ def matmul_geometry(shape, v):
     # the split goes across workgroups.
     kg = 2 if v["mfma"] and v["ks"] >= 2 and bk >= 8 else 1
     wgs = v["ks"] // kg
+    # Register budget of the compiled instances: two wave groups leave room
+    # for 64 accumulators per lane; a 128x128 wave tile with 16-deep K-tiles
+    # unrolled 8 times on one LDS stage does not fit; a VALU tile that stages
+    # the next K-tile in registers (dbuf) fits (rm + rn) * unroll <= 512.
+    if v["mfma"]:
+        ok = ok and (kg == 1 or acc <= 64) and not (
+            acc == 256 and not v["dbuf"] and bk == 16 and uf == 8)
+    else:
+        ok = ok and (not v["dbuf"] or (t0 + t1) * uf <= 512)
+    # vec = 4 (16-byte operand loads) needs rows of A (K) or B (N) in whole
+    # 16-byte groups
+    ok = ok and (v["vec"] == 1 or K % 4 == 0 or N % 4 == 0)
     lds = max(stages * stage, bm * bn if kg > 1 else 0) * 4
     nkt = _cdiv(K, bk)
     grid = _cdiv(M, bm) * _cdiv(N, bn) * wgs

@@ -40,6 +40,7 @@ STATUS_NAMES = {0: "DS_OK", -1: "DS_EINVAL", -2: "DS_EUNSUPPORTED", -3: "DS_EINV
 
 DS_OP_CONV2D_NCHW = 1
 DS_OP_MATMUL_RM = 2
+DS_KERNEL_CONV_VALU, DS_KERNEL_CONV_MFMA, DS_KERNEL_MM_VALU, DS_KERNEL_MM_MFMA = 1, 2, 3, 4
 DS_MAX_KNOBS = 12
 DS_MAX_REPEATS = 64
 DS_NOALLOC_MAX_FLOATS = 8388608   # kernel_run_noalloc: split partials capacity
@@ -57,6 +58,18 @@ class ds_geometry(C.Structure):
     _fields_ = [("valid", C.c_int32), ("threads", C.c_int32), ("grid", C.c_int64),
                 ("lds_bytes", C.c_int32), ("acc", C.c_int32), ("unroll_eff", C.c_int32),
                 ("t0", C.c_int32), ("t1", C.c_int32), ("red", C.c_int32), ("chunks", C.c_int64)]
+
+
+class ds_kernel_info(C.Structure):
+    _fields_ = [("family", C.c_int32), ("nparams", C.c_int32), ("params", C.c_int32 * 6),
+                ("instance", C.c_int32), ("threads", C.c_int32), ("grid", C.c_int64),
+                ("lds_bytes", C.c_int32), ("splits", C.c_int32), ("args_hash", C.c_uint64),
+                ("num_regs", C.c_int32), ("max_threads_per_block", C.c_int32),
+                ("local_bytes", C.c_int64), ("static_lds_bytes", C.c_int64)]
+
+    def as_dict(self):
+        return {f: (list(getattr(self, f))[: self.nparams] if f == "params" else getattr(self, f))
+                for f, _ in self._fields_}
 
 
 class ds_measure_cfg(C.Structure):
@@ -144,6 +157,10 @@ SIGNATURES = {
     "ansor_draw": (C.c_int, [C.c_void_p, C.c_uint64, C.c_int, C.POINTER(ds_sched),
                              C.POINTER(C.c_int)]),
     "sched_has_kernel": (C.c_int, [C.c_void_p, C.POINTER(ds_sched)]),
+    "sched_space_programs": (C.c_int, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_int32),
+                                       C.POINTER(C.c_uint64), C.c_int64, C.POINTER(C.c_int64)]),
+    "sched_kernel_info": (C.c_int, [C.c_void_p, C.POINTER(ds_sched), C.c_int,
+                                    C.POINTER(ds_kernel_info)]),
     "kernel_run": (C.c_int, [C.c_int, C.POINTER(ds_sched), C.c_void_p, C.c_void_p, C.c_void_p,
                              C.c_void_p]),
     "kernel_run_noalloc": (C.c_int, [C.c_int, C.POINTER(ds_sched), C.c_void_p, C.c_void_p,
@@ -349,6 +366,28 @@ class Space:
 
     def has_kernel(self, idx):
         return bool(check("sched_has_kernel", lib.sched_has_kernel(self.h, C.byref(self.sched(idx)))))
+
+    def kernel_info(self, idx, with_attrs=False):
+        """Compiled instance, launch geometry and argument hash of a valid point."""
+        out = ds_kernel_info()
+        check("sched_kernel_info", lib.sched_kernel_info(self.h, C.byref(self.sched(idx)),
+                                                         int(with_attrs), C.byref(out)))
+        return out.as_dict()
+
+    def programs(self):
+        """(keys, instances, args_hashes) of every valid point, key order (numpy)."""
+        import numpy as np
+        n = C.c_int64()
+        check("sched_space_programs", lib.sched_space_programs(self.h, None, None, None, 0,
+                                                               C.byref(n)))
+        keys = np.zeros(max(1, n.value), np.uint64)
+        inst = np.zeros(max(1, n.value), np.int32)
+        hashes = np.zeros(max(1, n.value), np.uint64)
+        check("sched_space_programs", lib.sched_space_programs(
+            self.h, keys.ctypes.data_as(C.POINTER(C.c_uint64)),
+            inst.ctypes.data_as(C.POINTER(C.c_int32)),
+            hashes.ctypes.data_as(C.POINTER(C.c_uint64)), n.value, C.byref(n)))
+        return keys[: n.value], inst[: n.value], hashes[: n.value]
 
     def draw(self, seed, n):
         out = (ds_sched * max(1, n))()

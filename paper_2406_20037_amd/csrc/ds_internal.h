@@ -146,6 +146,10 @@ inline int mm_group_rows(int tiles_m, int tiles_n, int ks, int bm, int bn) {
 
 struct Plan {
     const void *func = nullptr;
+    int family = 0;           // DS_KERNEL_* of the selected instance
+    int nparams = 0;
+    int params[6] = {0, 0, 0, 0, 0, 0};   // its template parameters
+    int slot = -1;            // its slot in the family's instance table
     int threads = 0;
     int64_t grid = 0;
     int lds = 0;
@@ -164,7 +168,7 @@ int launch_plan(const Plan &plan, hipStream_t stream);
 
 // Kernel instance lookup (compiled template instances).
 const void *conv_valu_instance(int kpt, int ppt, int uf, int lds);
-const void *conv_mfma_instance(int tkb, int npb, int uf, int lds);
+const void *conv_mfma_instance(int tkb, int npb, int d, int lds);
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf);
 const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf, int kg);
 int count_instances();

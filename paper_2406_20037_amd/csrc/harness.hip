@@ -14,6 +14,8 @@
 
 namespace ds {
 
+const Space &space_of(const ds_space *s);
+
 const void *g_conv_valu[kConvValuSlots];
 const void *g_conv_mfma[kConvMfmaSlots];
 const void *g_mm_valu[kMmValuSlots];
@@ -420,10 +422,10 @@ const void *conv_valu_instance(int kpt, int ppt, int uf, int lds) {
     return g_conv_valu[((a * 5 + b) * 5 + c) * 2 + lds];
 }
 
-const void *conv_mfma_instance(int tkb, int npb, int uf, int lds) {
-    const int a = log2_exact(tkb), b = log2_exact(npb), c = log2_exact(uf);
-    if (a < 0 || a > 2 || b < 0 || b > 6 || c < 0 || c > 4 || (lds & ~1)) return nullptr;
-    return g_conv_mfma[((a * 7 + b) * 5 + c) * 2 + lds];
+const void *conv_mfma_instance(int tkb, int npb, int d, int lds) {
+    const int a = log2_exact(tkb), b = log2_exact(npb);
+    if (a < 0 || a > 2 || b < 0 || b > 6 || d < 1 || d > 3 || (lds & ~1)) return nullptr;
+    return g_conv_mfma[((a * 7 + b) * 3 + d - 1) * 2 + lds];
 }
 
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf) {
@@ -498,7 +500,9 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         // tile is at least 16 columns wide: rows start at the 16-byte boundary
         // at or before the tile's first column (up to 3 more columns, rounded
         // to 4); otherwise rows hold exactly the tile's input columns
-        const bool halo16 = a.W % 4 == 0 && a.tw * a.st >= 16;
+        // (only with 16-byte copies, vec = 4)
+        const int vec = sp.value(s->idx, 8);
+        const bool halo16 = vec == 4 && a.W % 4 == 0 && a.tw * a.st >= 16;
         a.ws = halo16 ? int(cdiv64(int64_t(a.tw - 1) * a.st + a.S + 3, 4) * 4)
                       : (a.tw - 1) * a.st + a.S;
         a.npx = a.th * a.tw;
@@ -511,9 +515,12 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.f_s = make_fastdiv(a.S);
         a.f_wrow = make_fastdiv(a.wrow);
         // bit 0: weight rows staged 16 bytes per lane; bit 1: halo rows too;
-        // bit 2: aligned halo layout
-        a.w4 = ((a.C * a.R * a.S) % 4 == 0 && (a.tc * a.R * a.S) % 4 == 0 && a.wrow % 4 == 0 &&
-                reinterpret_cast<uintptr_t>(w) % 16 == 0 ? 1 : 0) |
+        // bit 2: aligned halo layout (16-byte copies only with vec = 4, and
+        // only from 16-byte aligned operands)
+        a.w4 = (vec == 4 && (a.C * a.R * a.S) % 4 == 0 && (a.tc * a.R * a.S) % 4 == 0 &&
+                        a.wrow % 4 == 0 && reinterpret_cast<uintptr_t>(w) % 16 == 0
+                    ? 1
+                    : 0) |
                (halo16 && (int64_t(a.tk) * a.wrow) % 4 == 0 &&
                         reinterpret_cast<uintptr_t>(x) % 16 == 0
                     ? 2
@@ -523,6 +530,13 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.buf = int(cdiv64(int64_t(a.tk) * a.wrow + int64_t(a.tc) * a.hs * a.ws + 1, 4) * 4);
         plan.func = mfma ? conv_mfma_instance(g.t0, g.t1, g.unroll_eff, lds)
                          : conv_valu_instance(g.t0, g.t1, g.unroll_eff, lds);
+        plan.family = mfma ? DS_KERNEL_CONV_MFMA : DS_KERNEL_CONV_VALU;
+        plan.nparams = 4;
+        const int pr[4] = {g.t0, g.t1, g.unroll_eff, lds};
+        std::memcpy(plan.params, pr, sizeof pr);
+        plan.slot = mfma ? ((log2_exact(g.t0) * 7 + log2_exact(g.t1)) * 3 + g.unroll_eff - 1) * 2 + lds
+                         : ((log2_exact(g.t0) * 5 + log2_exact(g.t1)) * 5 + log2_exact(g.unroll_eff)) *
+                                   2 + lds;
         plan.splits = a.ks > 1 ? int(cdiv64(a.chunks, a.cps)) : 1;
         plan.y_elems = int64_t(a.N) * a.K * a.P * a.Q;
     } else {
@@ -536,12 +550,22 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         a.tiles_n = int(cdiv64(a.N, bn));
         a.nkt = int(g.chunks);
         a.kps = int(cdiv64(a.nkt, a.ks));
-        a.vecA = (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
-        a.vecB = (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
+        // 16-byte operand loads only with vec = 4 (and aligned operands)
+        const int vec = sp.value(s->idx, 7);
+        a.vecA = vec == 4 && (a.K % 4 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0);
+        a.vecB = vec == 4 && (a.N % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
         a.direct = a.vecA && a.vecB && a.M % bm == 0 && a.N % bn == 0 && a.K % bk == 0;
         a.gm = mm_group_rows(a.tiles_m, a.tiles_n, a.ks, bm, bn);
         plan.func = mfma ? mm_mfma_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf, kg)
                          : mm_valu_instance(g.t0, g.t1, bk, g.unroll_eff, dbuf);
+        plan.family = mfma ? DS_KERNEL_MM_MFMA : DS_KERNEL_MM_VALU;
+        plan.nparams = mfma ? 6 : 5;
+        const int pr[6] = {g.t0, g.t1, bk, g.unroll_eff, dbuf, kg};
+        std::memcpy(plan.params, pr, sizeof pr);
+        const int lb = log2_exact(bk) - 2, lu = log2_exact(g.unroll_eff);
+        plan.slot = mfma ? ((((log2_exact(g.t0) - 4) * 4 + (log2_exact(g.t1) - 4)) * 5 + lb) * 7 + lu) *
+                                   4 + dbuf * 2 + (kg - 1)
+                         : (((log2_exact(g.t0) * 5 + log2_exact(g.t1)) * 5 + lb) * 7 + lu) * 2 + dbuf;
         plan.splits = a.ks > 1 ? int(cdiv64(a.nkt, a.kps)) : 1;
         plan.y_elems = int64_t(a.M) * a.N;
     }
@@ -968,6 +992,80 @@ int sched_has_kernel(const ds_space *space, const ds_sched *s) {
     const int rc = make_plan(s, nullptr, nullptr, nullptr, plan);
     if (rc == DS_OK) return 1;
     return rc == DS_EUNSUPPORTED ? 0 : rc;
+}
+
+int sched_kernel_info(const ds_space *space, const ds_sched *s, int with_attrs,
+                      ds_kernel_info *out) {
+    if (!out) {
+        set_error("out is null");
+        return DS_EINVAL;
+    }
+    std::memset(out, 0, sizeof *out);
+    const int v = sched_valid(space, s);
+    if (v < 0) return v;
+    if (v == 0) {
+        set_error("schedule is not a valid point of its search space");
+        return DS_EINVALID_SCHED;
+    }
+    Plan plan;
+    int rc = make_plan(s, nullptr, nullptr, nullptr, plan);
+    if (rc != DS_OK) return rc;
+    out->family = plan.family;
+    out->nparams = plan.nparams;
+    for (int i = 0; i < 6; ++i) out->params[i] = plan.params[i];
+    out->instance = plan.family * 4096 + plan.slot;
+    out->threads = plan.threads;
+    out->grid = plan.grid;
+    out->lds_bytes = plan.lds;
+    out->splits = plan.splits;
+    // FNV-1a over the kernel's argument block (buffer pointers are null here)
+    const unsigned char *b = plan.op == DS_OP_CONV2D_NCHW
+                                 ? reinterpret_cast<const unsigned char *>(&plan.conv)
+                                 : reinterpret_cast<const unsigned char *>(&plan.mm);
+    const size_t nb = plan.op == DS_OP_CONV2D_NCHW ? sizeof plan.conv : sizeof plan.mm;
+    uint64_t h = 1469598103934665603ull;
+    for (size_t i = 0; i < nb; ++i) h = (h ^ b[i]) * 1099511628211ull;
+    out->args_hash = h;
+    if (with_attrs) {
+        hipFuncAttributes fa;
+        if (!hip_ok(hipFuncGetAttributes(&fa, plan.func), "hipFuncGetAttributes")) return DS_EHIP;
+        out->num_regs = fa.numRegs;
+        out->max_threads_per_block = fa.maxThreadsPerBlock;
+        out->local_bytes = int64_t(fa.localSizeBytes);
+        out->static_lds_bytes = int64_t(fa.sharedSizeBytes);
+    }
+    return DS_OK;
+}
+
+int sched_space_programs(const ds_space *space, uint64_t *keys, int32_t *instances,
+                         uint64_t *args_hashes, int64_t cap, int64_t *n_out) {
+    if (!space || !n_out || cap < 0 || (cap > 0 && (!keys || !instances || !args_hashes))) {
+        set_error("bad arguments");
+        return DS_EINVAL;
+    }
+    const Space &sp = space_of(space);
+    if (sp.op != DS_OP_CONV2D_NCHW && sp.op != DS_OP_MATMUL_RM) {
+        set_error("a generic lattice has no kernel");
+        return DS_EINVAL;
+    }
+    int64_t n = 0;
+    int32_t idx[DS_MAX_KNOBS] = {0};
+    for (uint64_t k = 0; k < sp.size; ++k) {
+        sp.from_key(k, idx);
+        if (!sp.geometry(idx).valid) continue;
+        if (n < cap) {
+            const ds_sched s = make_sched(sp, idx);
+            ds_kernel_info info;
+            const int rc = sched_kernel_info(space, &s, 0, &info);
+            if (rc != DS_OK) return rc;
+            keys[n] = k;
+            instances[n] = info.instance;
+            args_hashes[n] = info.args_hash;
+        }
+        ++n;
+    }
+    *n_out = n;
+    return DS_OK;
 }
 
 void ds_shutdown(void) {

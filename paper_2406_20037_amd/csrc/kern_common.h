@@ -28,7 +28,7 @@ __device__ __forceinline__ void store_out(float *p, float v) { __builtin_nontemp
 
 // Instance table sizes (one slot per template-parameter tuple).
 constexpr int kConvValuSlots = 7 * 5 * 5 * 2;   // KPT, PPT, UF, LDS
-constexpr int kConvMfmaSlots = 3 * 7 * 5 * 2;   // TKB, NPB, UF, LDS
+constexpr int kConvMfmaSlots = 3 * 7 * 3 * 2;   // TKB, NPB, D, LDS
 constexpr int kMmValuSlots = 5 * 5 * 5 * 7 * 2; // RM, RN, BK, UF, DB
 constexpr int kMmMfmaSlots = 4 * 4 * 5 * 7 * 2 * 2; // WM, WN, BK, UF, DB, KG
 
@@ -45,6 +45,22 @@ constexpr bool conv_uf_reachable(int body, int uf) {
     const int us[3] = {16, 64, 512};
     for (int u : us)
         if (cmin(16, p2floor(cmax(1, u / body))) == uf) return true;
+    return false;
+}
+
+// Read-ahead depth of the MFMA conv's group loop for an unroll factor u of
+// conv_uf (1..16): 1 below 4, 2 below 16, 3 at 16.
+constexpr int conv_mfma_depth(int u) { return u >= 16 ? 3 : (u >= 4 ? 2 : 1); }
+
+// Depths the lattice can produce for TKB x NPB blocks, and that fit: the
+// D+1 operand sets (4 TKB + 4 NPB floats each) stay within 96 registers.
+constexpr bool conv_mfma_depth_ok(int tkb, int npb, int d) {
+    if ((d + 1) * 4 * (tkb + npb) > 96) return d == 1;
+    const int body = tkb * npb;
+    if (d == 1) return true;
+    const int us[3] = {16, 64, 512};
+    for (int u : us)
+        if (conv_mfma_depth(cmin(16, p2floor(cmax(1, u / body)))) == d) return true;
     return false;
 }
 

@@ -15,8 +15,9 @@
 //              NPB 16x16 blocks.  Lane group g (lanes
 //              16g..16g+15) feeds reduction steps kr = 16*j + 4*g + v, v < 4,
 //              for both operands, so a 16-byte LDS read gives four steps of A.
-//              Operands of the next 16-step group are read while the MFMAs of
-//              the current one run.
+//              The operands of the D next 16-step groups are read while the
+//              MFMAs of the current one run (D, 1 to 3, is the unroll knob's
+//              read-ahead depth: D+1 operand sets, loop unrolled by D+1).
 //
 // LDS layout (lds=1): [weights tk x wrow][input halo tc x hs x ws][zero] per buffer,
 //                    then [table red][weight sources tk x wrow][halo sources tc x hs x ws]
@@ -317,12 +318,17 @@ __device__ __forceinline__ void stage_init(const ConvArgs &a, float *smem, int k
     __syncthreads();
 }
 
+// WHOLE: the workgroup is whole waves (always for conv_mfma).  Only then are
+// the asynchronous copies used; the register-staged fallback is left out of
+// such kernels, because its loads into registers, merged into the chunk loop,
+// make the compiler wait for every copy in flight before the next LDS read.
+template <bool WHOLE>
 __device__ __forceinline__ void stage_to(const ConvArgs &a, float *smem, int b, int n, int kt, int pt,
                                          int qt, int ci, const int *wsrc, const int *xsrc) {
     float *wt = smem + b * a.buf;
     float *xs = wt + a.tk * a.wrow;
     const int c0 = ci * a.tc;
-    if ((blockDim.x & 63) == 0) {
+    if (WHOLE || (blockDim.x & 63) == 0) {
         if (c0 + a.tc <= a.C) dma_chunk_tab(a, n, kt, c0, wsrc, xsrc, wt, xs);
         else dma_chunk(a, n, kt, pt, qt, c0, wt, xs);      // channel tail
     } else {
@@ -373,11 +379,12 @@ struct RegStage {
             __builtin_amdgcn_global_load_lds(DS_GLOBAL(base + off), DS_LOCAL(dst), 4, 0, 0);
     }
 
+    template <bool WHOLE>
     __device__ __forceinline__ void to(const ConvArgs &a, float *smem, int b, int n, int kt, int pt,
                                        int qt, int ci, const int *wsrc, const int *xsrc) const {
         const int c0 = ci * a.tc;
         if (!(onw || onh) || c0 + a.tc > a.C) {
-            stage_to(a, smem, b, n, kt, pt, qt, ci, wsrc, xsrc);
+            stage_to<WHOLE>(a, smem, b, n, kt, pt, qt, ci, wsrc, xsrc);
             return;
         }
         float *wt = smem + b * a.buf;
@@ -410,6 +417,36 @@ struct RegStage {
         }
     }
 };
+
+// Software pipeline over the 16-step groups of a chunk with D groups read
+// ahead: operand set r%(D+1) holds group r; the reads of group g+D are issued
+// before the MFMAs of group g, so those MFMAs need not wait for them.  The
+// loop is unrolled by D+1, so every set index is a compile-time constant and
+// the body has no branch (its wait counts stay exact).  Reads past the last
+// group re-read the last group into a set that is never consumed.
+template <int D, class Ops, class Load, class Mma>
+__device__ __forceinline__ void group_ring(int ngroups, Load &&load, Mma &&mma) {
+    constexpr int RG = D + 1;
+    Ops o[RG];
+#pragma unroll
+    for (int r = 0; r < D; ++r) load(min(r, ngroups - 1), o[r]);
+    int kg = 0;
+    for (; kg + RG <= ngroups; kg += RG) {
+#pragma unroll
+        for (int r = 0; r < RG; ++r) {
+            load(min(kg + r + D, ngroups - 1), o[(r + D) % RG]);
+            mma(o[r]);
+        }
+    }
+    // fewer than RG groups remain; groups kg .. kg+D-1 are loaded
+#pragma unroll
+    for (int r = 0; r < RG - 1; ++r) {
+        if (kg + r < ngroups) {
+            if (kg + r + D < ngroups) load(kg + r + D, o[(r + D) % RG]);
+            mma(o[r]);
+        }
+    }
+}
 
 template <int KPT, int PPT, int UF, int LDS>
 __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
@@ -453,7 +490,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
     if (LDS) {
         stage_init(a, smem, kt, pt, qt, wsrc, xsrc);
         rs.init(a, wsrc, xsrc);
-        rs.to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
+        rs.template to<false>(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
     }
     __builtin_amdgcn_s_setprio(0);
 
@@ -469,7 +506,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
                 // that issue MFMAs back to back their vector instructions
                 // otherwise wait for issue slots
                 __builtin_amdgcn_s_setprio(3);
-                rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+                rs.template to<false>(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
                 __builtin_amdgcn_s_setprio(0);
             }
             const float *wt = smem + bi * a.buf;
@@ -533,7 +570,7 @@ __global__ __launch_bounds__(256) void conv_valu(ConvArgs a) {
     }
 }
 
-template <int TKB, int NPB, int UF, int LDS>
+template <int TKB, int NPB, int D, int LDS>
 __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
     extern __shared__ float smem[];
     int n, z, kt, pt, qt;
@@ -575,11 +612,10 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
     if (LDS) {
         stage_init(a, smem, kt, pt, qt, wsrc, xsrc);
         rs.init(a, wsrc, xsrc);
-        rs.to(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
+        rs.template to<true>(a, smem, 0, n, kt, pt, qt, ci0, wsrc, xsrc);
     }
     __builtin_amdgcn_s_setprio(0);
 
-    constexpr int UG = UF >= 4 ? UF / 4 : 1;   // 16-step groups unrolled
     const int RS = a.R * a.S;
     const int crs = a.C * RS;
     const int ngroups = a.red / 16;
@@ -589,11 +625,11 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
             const int bi = (ci - ci0) & 1;
             chunk_barrier();
             if (ci + 1 < ci1) {
-                // the copies are issued at raised wave priority: next to waves
-                // that issue MFMAs back to back their vector instructions
-                // otherwise wait for issue slots
+                // the next chunk's copies go to the other buffer, issued at
+                // raised wave priority: next to waves that issue MFMAs back to
+                // back their vector instructions otherwise wait for issue slots
                 __builtin_amdgcn_s_setprio(3);
-                rs.to(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
+                rs.template to<true>(a, smem, bi ^ 1, n, kt, pt, qt, ci + 1, wsrc, xsrc);
                 __builtin_amdgcn_s_setprio(0);
             }
             const float *wt = smem + bi * a.buf;
@@ -606,23 +642,30 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
                 const float *ap[TKB];
 #pragma unroll
                 for (int i = 0; i < TKB; ++i) ap[i] = wt + (i * 16 + li) * a.wrow + 4 * lg;
-                // Two groups per iteration with two named operand sets: the
-                // reads of group kg+1 are issued before the MFMAs of group kg
-                // (LDS returns in order, so those MFMAs need not wait for them).
-                auto load = [&](int kg, floatx4 (&av)[TKB], float (&bv)[4][NPB]) {
+                struct Ops {
+                    floatx4 a[TKB];
+                    float b[4][NPB];
+                };
+                auto load = [&](int kg, Ops &o) {
                     const int kb = kg * 16 + 4 * lg;
-                    const int4 off = *reinterpret_cast<const int4 *>(tab + kb);
-                    const int offv[4] = {off.x, off.y, off.z, off.w};
+                    // the offsets are read as float-typed data: an int-typed
+                    // LDS read makes the compiler wait for every copy in flight
+                    // (the buffers this loop reads are already complete: the
+                    // chunk barrier waited for their copies)
+                    const floatx4 offf =
+                        *reinterpret_cast<const floatx4 *>(reinterpret_cast<const float *>(tab) + kb);
+                    const int offv[4] = {__float_as_int(offf[0]), __float_as_int(offf[1]),
+                                         __float_as_int(offf[2]), __float_as_int(offf[3])};
 #pragma unroll
                     for (int i = 0; i < TKB; ++i)
-                        av[i] = *reinterpret_cast<const floatx4 *>(ap[i] + kg * 16);
+                        o.a[i] = *reinterpret_cast<const floatx4 *>(ap[i] + kg * 16);
 #pragma unroll
                     for (int v = 0; v < 4; ++v)
 #pragma unroll
                         for (int b = 0; b < NPB; ++b)
-                            bv[v][b] = *reinterpret_cast<const float *>(bp[b] + offv[v]);
+                            o.b[v][b] = *reinterpret_cast<const float *>(bp[b] + offv[v]);
                 };
-                auto mma = [&](const floatx4 (&av)[TKB], const float (&bv)[4][NPB]) {
+                auto mma = [&](const Ops &o) {
 #pragma unroll
                     for (int v = 0; v < 4; ++v)
 #pragma unroll
@@ -630,36 +673,22 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
 #pragma unroll
                             for (int b = 0; b < NPB; ++b)
                                 acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                                    av[i][v], bv[v][b], acc[i][b], 0, 0, 0);
+                                    o.a[i][v], o.b[v][b], acc[i][b], 0, 0, 0);
                 };
-                // The loop body has no branch: the wait counts stay exact, so
-                // the MFMAs of one group never wait for the next group's reads.
-                floatx4 a0[TKB], a1[TKB];
-                float b0[4][NPB], b1[4][NPB];
-                load(0, a0, b0);
-                int kg = 0;
-                for (; kg + 2 < ngroups; kg += 2) {
-                    load(kg + 1, a1, b1);
-                    mma(a0, b0);
-                    load(kg + 2, a0, b0);
-                    mma(a1, b1);
-                }
-                if (kg + 1 < ngroups) {
-                    load(kg + 1, a1, b1);
-                    mma(a0, b0);
-                    mma(a1, b1);
-                } else {
-                    mma(a0, b0);
-                }
+                group_ring<D, Ops>(ngroups, load, mma);
             }
         } else {
             if (ci == ci0) __syncthreads();
             const float *xc = a.x + ((size_t)n * a.C + c0) * a.H * a.W;
-            // Software pipeline: the operands of the next 16-step group are
+            // Software pipeline: the operands of the D next 16-step groups are
             // loaded while the MFMAs of the current one run.  Positions that
             // read zero load the zero in device memory, so no select waits on
             // a load.
-            auto gload = [&](int kg, float (&A)[4][TKB], float (&B)[4][NPB]) {
+            struct Ops {
+                float A[4][TKB];
+                float B[4][NPB];
+            };
+            auto gload = [&](int kg, Ops &o) {
                 const int kb = kg * 16 + 4 * lg;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -673,42 +702,27 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
                     for (int i = 0; i < TKB; ++i) {
                         const int k = kt * a.tk + i * 16 + li;
                         const bool wok = cok && k < a.K;
-                        A[v][i] = *(wok ? gptr(a.w + (size_t)k * crs + c0 * RS + kr) : gptr(kZero));
+                        o.A[v][i] = *(wok ? gptr(a.w + (size_t)k * crs + c0 * RS + kr) : gptr(kZero));
                     }
 #pragma unroll
                     for (int b = 0; b < NPB; ++b) {
                         const int iy = iy0[b] + r, ix = ix0[b] + s;
                         const bool ok = cok && pv[b] && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
-                        B[v][b] = *(ok ? gptr(xc + goff + iy0[b] * a.W + ix0[b]) : gptr(kZero));
+                        o.B[v][b] = *(ok ? gptr(xc + goff + iy0[b] * a.W + ix0[b]) : gptr(kZero));
                     }
                 }
             };
-            auto gmma = [&](const float (&A)[4][TKB], const float (&B)[4][NPB]) {
+            auto gmma = [&](const Ops &o) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
 #pragma unroll
                     for (int i = 0; i < TKB; ++i)
 #pragma unroll
                         for (int b = 0; b < NPB; ++b)
-                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[v][i], B[v][b],
+                            acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.A[v][i], o.B[v][b],
                                                                             acc[i][b], 0, 0, 0);
             };
-            float A0[4][TKB], B0[4][NPB], A1[4][TKB], B1[4][NPB];
-            gload(0, A0, B0);
-            int kg = 0;
-            for (; kg + 2 < ngroups; kg += 2) {
-                gload(kg + 1, A1, B1);
-                gmma(A0, B0);
-                gload(kg + 2, A0, B0);
-                gmma(A1, B1);
-            }
-            if (kg + 1 < ngroups) {
-                gload(kg + 1, A1, B1);
-                gmma(A0, B0);
-                gmma(A1, B1);
-            } else {
-                gmma(A0, B0);
-            }
+            group_ring<D, Ops>(ngroups, gload, gmma);
         }
     }
 
@@ -729,7 +743,7 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
 
 // ---- instance registry --------------------------------------------------------
 // conv_valu slots: ((log2 KPT * 5 + log2 PPT) * 5 + log2 UF) * 2 + LDS
-// conv_mfma slots: ((log2 TKB * 7 + log2 NPB) * 5 + log2 UF) * 2 + LDS
+// conv_mfma slots: ((log2 TKB * 7 + log2 NPB) * 3 + D - 1) * 2 + LDS
 constexpr int kValuSlots = kConvValuSlots;
 constexpr int kMfmaSlots = kConvMfmaSlots;
 
@@ -755,10 +769,11 @@ void reg_valu() {
 
 template <int I>
 void reg_mfma() {
-    constexpr int lds = I % 2, iuf = (I / 2) % 5, inpb = (I / 10) % 7, itkb = I / 70;
-    constexpr int TKB = 1 << itkb, NPB = 1 << inpb, UF = 1 << iuf;
-    if constexpr (TKB * NPB <= 32 && conv_uf_reachable(TKB * NPB, UF) && I % DS_NSLICES == DS_SLICE)
-        g_conv_mfma[I] = reinterpret_cast<const void *>(&conv_mfma<TKB, NPB, UF, lds>);
+    constexpr int lds = I % 2, D = (I / 2) % 3 + 1, inpb = (I / 6) % 7, itkb = I / 42;
+    constexpr int TKB = 1 << itkb, NPB = 1 << inpb;
+    if constexpr (TKB * NPB <= 32 && conv_mfma_depth_ok(TKB, NPB, D) &&
+                  I % DS_NSLICES == DS_SLICE)
+        g_conv_mfma[I] = reinterpret_cast<const void *>(&conv_mfma<TKB, NPB, D, lds>);
 }
 
 template <size_t... I>

@@ -21,9 +21,10 @@ const int32_t kSplit[] = {1, 2, 4, 8};
 const int32_t kMmTile[] = {16, 32, 64, 128, 256};
 const int32_t kMmBk[] = {4, 8, 16, 32, 64};
 const int32_t kOnOff[] = {0, 1};
+const int32_t kVec[] = {1, 4};
 
-const char *kConvNames[] = {"tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma"};
-const char *kMmNames[] = {"bm", "bn", "bk", "unroll", "dbuf", "mfma", "ks"};
+const char *kConvNames[] = {"tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma", "vec"};
+const char *kMmNames[] = {"bm", "bn", "bk", "unroll", "dbuf", "mfma", "ks", "vec"};
 const char *kGenericNames[] = {"p0", "p1", "p2", "p3", "p4", "p5",
                                "p6", "p7", "p8", "p9", "p10", "p11"};
 
@@ -64,7 +65,7 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
                   st = sh[7], pd = sh[8];
     const int64_t P = conv_out_dim(H, R, st, pd), Q = conv_out_dim(W, S, st, pd);
     const int tk = v[0], th = v[1], tw = v[2], tc = v[3], unroll = v[4], lds = v[5], ks = v[6],
-              mfma = v[7];
+              mfma = v[7], vec = v[8];
     Geometry g;
     const int npx = th * tw;
     const int outs = tk * npx;
@@ -109,10 +110,10 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         g.t0 = tkb;
         g.t1 = npb;
     }
-    // aligned halo layout (image rows of whole 16-byte groups, tiles of at
-    // least 16 input columns): rows start at the 16-byte boundary at or before
-    // the tile's first column, up to 3 more columns, rounded to 4
-    const bool halo16 = W % 4 == 0 && int64_t(tw) * st >= 16;
+    // aligned halo layout (16-byte copies, image rows of whole 16-byte groups,
+    // tiles of at least 16 input columns): rows start at the 16-byte boundary
+    // at or before the tile's first column, up to 3 more columns, rounded to 4
+    const bool halo16 = vec == 4 && W % 4 == 0 && int64_t(tw) * st >= 16;
     const int64_t hs = int64_t(th - 1) * st + R;
     const int64_t ws = halo16 ? cdiv(int64_t(tw - 1) * st + S + 3, 4) * 4 : int64_t(tw - 1) * st + S;
     g.chunks = std::max<int64_t>(1, cdiv(C, tc));
@@ -130,6 +131,26 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
     g.lds_bytes = int(std::min<int64_t>(lds_bytes, INT32_MAX));
     g.grid = N * ks * cdiv(K, tk) * cdiv(P, th) * cdiv(Q, tw);
     g.unroll_eff = unroll == 0 ? 1 : std::min(16, pow2_floor(std::max(1, unroll / body)));
+    if (mfma) {
+        // The MFMA family unrolls its group loop by its read-ahead depth D
+        // (1..3); its D+1 operand sets hold 4*(tkb + npb) floats each.  Register
+        // budget of the compiled instances (no spill): at most 96 such floats,
+        // or 192 with D = 1.
+        g.unroll_eff = g.unroll_eff >= 16 ? 3 : (g.unroll_eff >= 4 ? 2 : 1);
+        const int ring = (g.unroll_eff + 1) * 4 * (g.t0 + g.t1);
+        ok = ok && (ring <= 96 || (g.unroll_eff == 1 && ring <= 192));
+    } else {
+        // register budget: 64 accumulators on the global path fit only a
+        // loop unrolled less than 8 times
+        ok = ok && !(lds == 0 && g.acc == 64 && g.unroll_eff >= 8);
+    }
+    // vec = 4 (16-byte global -> LDS copies) needs LDS staging by whole waves
+    // and at least one operand whose staged rows are whole 16-byte groups
+    if (vec == 4) {
+        const bool w16 = (C * R * S) % 4 == 0 && (int64_t(tc) * R * S) % 4 == 0 && wrow % 4 == 0;
+        const bool h16 = halo16 && (int64_t(tk) * wrow) % 4 == 0;
+        ok = ok && lds && g.threads % 64 == 0 && (w16 || h16);
+    }
     g.valid = ok && lds_bytes <= kLdsLimit && g.threads <= kThreadsLimit && ks <= g.chunks &&
               g.grid <= kGridLimit;
     return g;
@@ -137,7 +158,8 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
 
 Geometry mm_geometry(const int64_t *sh, const int32_t *v) {
     const int64_t M = sh[0], N = sh[1], K = sh[2];
-    const int bm = v[0], bn = v[1], bk = v[2], unroll = v[3], dbuf = v[4], mfma = v[5], ks = v[6];
+    const int bm = v[0], bn = v[1], bk = v[2], unroll = v[3], dbuf = v[4], mfma = v[5], ks = v[6],
+              vec = v[7];
     Geometry g;
     bool ok;
     int body, kstep;
@@ -178,6 +200,16 @@ Geometry mm_geometry(const int64_t *sh, const int32_t *v) {
     // workgroup, then the K-tiles between workgroups (partials + reduce)
     const int kg = mm_wave_groups(mfma, ks, bk);
     const int wgs = ks / kg;
+    // Register budget of the compiled instances (no spill): two wave groups
+    // (512 threads) leave half the registers per lane, so at most 64
+    // accumulators; a 128x128 wave tile with a 16-deep K-tile unrolled 8
+    // times and one LDS stage does not fit; a VALU tile whose next K-tile is
+    // staged through registers (dbuf) fits (rm + rn) * unroll <= 512.
+    if (mfma)
+        ok = ok && (kg == 1 || g.acc <= 64) &&
+             !(g.acc == 256 && !dbuf && bk == 16 && g.unroll_eff == 8);
+    else
+        ok = ok && (!dbuf || (g.t0 + g.t1) * g.unroll_eff <= 512);
     const int64_t lds = std::max<int64_t>(int64_t(mm_stages(bm, bn, bk, dbuf)) * (bm * bk + bk * bn),
                                           kg > 1 ? int64_t(bm) * bn : 0) * 4;
     g.lds_bytes = int(std::min<int64_t>(lds, INT32_MAX));
@@ -185,6 +217,9 @@ Geometry mm_geometry(const int64_t *sh, const int32_t *v) {
     g.chunks = cdiv(K, bk);
     g.grid = cdiv(M, bm) * cdiv(N, bn) * wgs;
     g.threads = 256 * kg;
+    // vec = 4 (16-byte operand loads) needs rows of A (K) or of B (N) in whole
+    // 16-byte groups
+    ok = ok && (vec == 1 || K % 4 == 0 || N % 4 == 0);
     g.valid = ok && lds <= kLdsLimit && g.threads <= kThreadsLimit && wgs <= g.chunks &&
               g.grid <= kGridLimit;
     return g;
@@ -269,8 +304,8 @@ int build_space(int op, const int64_t *sh, int shape_len, Space &sp) {
         for (int i = 0; i < 9; ++i) sp.shape[i] = sh[i];
         sp.values = {clipped(kPow2to64, K), clipped(kPow2to64, P), clipped(kPow2to64, Q),
                      clipped(kPow2to64, C), all_of(kUnroll), all_of(kOnOff),
-                     clipped(kSplit, C), all_of(kOnOff)};
-        sp.names.assign(kConvNames, kConvNames + 8);
+                     clipped(kSplit, C), all_of(kOnOff),       all_of(kVec)};
+        sp.names.assign(kConvNames, kConvNames + 9);
     } else if (op == DS_OP_MATMUL_RM) {
         if (shape_len != 3) {
             set_error("matmul shape has 3 entries, got %d", shape_len);
@@ -288,8 +323,8 @@ int build_space(int op, const int64_t *sh, int shape_len, Space &sp) {
         for (int i = 0; i < 3; ++i) sp.shape[i] = sh[i];
         sp.values = {clipped(kMmTile, M), clipped(kMmTile, N), clipped(kMmBk, K),
                      all_of(kUnroll),     all_of(kOnOff),      all_of(kOnOff),
-                     clipped(kSplit, K)};
-        sp.names.assign(kMmNames, kMmNames + 7);
+                     clipped(kSplit, K),  all_of(kVec)};
+        sp.names.assign(kMmNames, kMmNames + 8);
     } else {
         set_error("unknown op %d", op);
         return DS_EUNSUPPORTED;

@@ -170,7 +170,7 @@ def test_matmul_every_mfma_class_exact(torch_dev, lib):
         k = o.knobs(p)
         if k["mfma"] != 1:
             continue
-        cls = (k["bm"], k["bn"], k["bk"], k["dbuf"], k["ks"], k["unroll"] >= 16)
+        cls = (k["bm"], k["bn"], k["bk"], k["dbuf"], k["ks"], k["unroll"] >= 16, k["vec"])
         if cls in seen:
             continue
         seen.add(cls)
@@ -243,10 +243,10 @@ def test_reference_kernels(torch_dev, lib):
 
 
 MODEL_SCHEDULES = [
-    dict(tk=32, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1),
-    dict(tk=16, th=4, tw=16, tc=8, unroll=16, lds=1, ks=2, mfma=1),
-    dict(tk=8, th=4, tw=8, tc=8, unroll=16, lds=1, ks=1, mfma=0),
-    dict(tk=16, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1),
+    dict(tk=32, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1, vec=4),
+    dict(tk=16, th=4, tw=16, tc=8, unroll=16, lds=1, ks=2, mfma=1, vec=4),
+    dict(tk=8, th=4, tw=8, tc=8, unroll=16, lds=1, ks=1, mfma=0, vec=1),
+    dict(tk=16, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1, vec=1),
 ]
 
 
@@ -288,8 +288,8 @@ def test_model_layers_sampled(torch_dev, lib, name, op, sh, count):
     idx = np.unique(np.concatenate([rng.integers(0, r.n, 3000), [0, r.n - 1]])).astype(np.int64)
     ref = ok.conv2d_f64_points(x, w, sh, idx) if op == 1 else ok.matmul_f64_points(x, w, idx)
     scheds = MODEL_SCHEDULES if op == 1 else [
-        dict(bm=16, bn=64, bk=64, unroll=64, dbuf=1, mfma=0, ks=8),
-        dict(bm=16, bn=16, bk=16, unroll=16, dbuf=0, mfma=0, ks=1)]
+        dict(bm=16, bn=64, bk=64, unroll=64, dbuf=1, mfma=0, ks=8, vec=4),
+        dict(bm=16, bn=16, bk=16, unroll=16, dbuf=0, mfma=0, ks=1, vec=1)]
     seen = set()
     for want in scheds:
         p = nearest_valid(o, want)
@@ -312,7 +312,7 @@ def test_measure_and_parity_detection(torch_dev, lib):
     y = torch.empty(ref.size, device="cuda:0")
     good = to_dev(torch, ref)
     io = lib.make_io(xd, wd, y, good)
-    p = s.sched_of(tk=32, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1)
+    p = s.sched_of(tk=32, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1, vec=4)
     m = lib.ds_measure(p, io, lib.measure_cfg(repeat=7))
     assert m.status == 0 and m.n_repeats == 7 and 0 < m.median_ms < 10
     assert m.max_err <= 1e-4 * m.max_ref and m.nonfinite == 0

@@ -44,9 +44,9 @@ def close(torch, c):
 def test_two_streams_split_concurrently(env):
     torch, L = env
     a = conv_case(torch, L, (1, 64, 40, 40, 64, 3, 3, 1, 1),
-                  dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1))
+                  dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1, vec=4))
     b = conv_case(torch, L, (2, 32, 24, 24, 48, 3, 3, 1, 1),
-                  dict(tk=16, th=4, tw=8, tc=8, unroll=0, lds=1, ks=2, mfma=1))
+                  dict(tk=16, th=4, tw=8, tc=8, unroll=0, lds=1, ks=2, mfma=1, vec=4))
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     print("two streams", flush=True)
@@ -61,7 +61,7 @@ def test_two_streams_split_concurrently(env):
 def test_capture_after_the_workspace_exists(env):
     torch, L = env
     c = conv_case(torch, L, (1, 64, 40, 40, 64, 3, 3, 1, 1),
-                  dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1))
+                  dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1, vec=4))
     st = torch.cuda.Stream()
     # first call outside capture creates this stream's workspace
     L.kernel_run(L.DS_OP_CONV2D_NCHW, c["s"], c["x"], c["w"], c["y"], st)
@@ -84,7 +84,7 @@ def test_capture_after_the_workspace_exists(env):
 def test_capture_without_a_workspace_is_refused(env):
     torch, L = env
     c = conv_case(torch, L, (1, 32, 20, 20, 32, 3, 3, 1, 1),
-                  dict(tk=16, th=4, tw=16, tc=4, unroll=0, lds=1, ks=8, mfma=1))
+                  dict(tk=16, th=4, tw=16, tc=4, unroll=0, lds=1, ks=8, mfma=1, vec=4))
     st = torch.cuda.Stream()
     g = torch.cuda.CUDAGraph()
     err = None

@@ -55,18 +55,18 @@ def test_value_lists_named_shapes():
     assert s0.values[0] == [1, 2, 4, 8, 16, 32, 64]
     assert s0.values[1] == [1, 2, 4, 8, 16, 32] == s0.values[2]
     assert s0.values[3] == [1, 2, 4, 8, 16, 32, 64]
-    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1]]
-    assert s0.size() == 7 * 6 * 6 * 7 * 4 * 2 * 4 * 2
+    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1], [1, 4]]
+    assert s0.size() == 7 * 6 * 6 * 7 * 4 * 2 * 4 * 2 * 2
     s2 = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
     assert s2.values[1] == [1, 2, 4, 8, 16, 32, 64]       # P = 112
     assert s2.values[3] == [1, 2] and s2.values[6] == [1, 2]
     m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
     assert m.values == [[16, 32, 64, 128, 256]] * 2 + [[4, 8, 16, 32, 64], [0, 16, 64, 512],
-                                                         [0, 1], [0, 1], [1, 2, 4, 8]]
+                                                         [0, 1], [0, 1], [1, 2, 4, 8], [1, 4]]
     fc = sp.Space(sp.OP_MATMUL, (1, 1000, 2048))
     assert fc.values[0] == [16]                          # smallest value kept
     tiny = sp.Space(sp.OP_MATMUL, (3, 5, 2))
-    assert tiny.values[2] == [4] and tiny.values[6] == [1, 2]
+    assert tiny.values[2] == [4] and tiny.values[6] == [1, 2] and tiny.values[7] == [1, 4]
 
 
 def idx_of(space, **kv):
@@ -75,45 +75,78 @@ def idx_of(space, **kv):
 
 def test_conv_geometry_hand_computed():
     s = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
-    g = s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1))
+    g = s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1, vec=4))
     # 64 pixels -> one 16-pixel block per wave; 16 channels -> one block.
     # reduction 16*9 = 144 (a multiple of 16); weight rows padded to 148; halo
     # 10x10 (8 columns wide: no aligned layout); 4 chunks in one split -> two
     # buffers of 16*148 + 16*100 + 1 -> 3972 floats, + table, + one staging
-    # source per weight and halo position (2368 + 1600).
+    # source per weight and halo position (2368 + 1600).  Unroll 64 over one
+    # block per step -> u = 16 -> read-ahead depth 3 (ring 4 * 4 * 2 = 32).
     assert g == dict(valid=True, grid=4 * 7 * 7, threads=256,
                      lds_bytes=4 * (2 * 3972 + 144 + 2368 + 1600), acc=4,
-                     unroll_eff=16, t0=1, t1=1, red=144, chunks=4)
-    g = s.geometry(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0))
+                     unroll_eff=3, t0=1, t1=1, red=144, chunks=4)
+    # 4-byte copies: the same layout here (the halo is narrower than 16 columns)
+    assert s.geometry(idx_of(s, tk=16, th=8, tw=8, tc=16, unroll=64, lds=1, ks=1, mfma=1,
+                             vec=1)) == g
+    # unroll 16 with two 16x16 blocks per step -> u = 8 -> depth 2
+    g = s.geometry(idx_of(s, tk=32, th=8, tw=8, tc=16, unroll=16, lds=1, ks=1, mfma=1, vec=4))
+    assert g["valid"] and g["unroll_eff"] == 2 and (g["t0"], g["t1"]) == (2, 1)
+    g = s.geometry(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0, vec=1))
     # 128 pixels x 4 channels -> 256 threads, 2 channel groups of 2; unroll 16//2 = 8.
     assert g == dict(valid=True, grid=2 * 16 * 14 * 2, threads=256, lds_bytes=8 * 72, acc=2,
                      unroll_eff=8, t0=2, t1=1, red=72, chunks=8)
     # One pixel, 64 channels: one wave, one channel per lane; 32 chunks -> two
     # buffers of 64*18 + 2*3*3 + 1 = 1171 -> 1172 floats, + table, + sources.
-    g = s.geometry(idx_of(s, tk=64, th=1, tw=1, tc=2, unroll=0, lds=1, ks=1, mfma=0))
+    g = s.geometry(idx_of(s, tk=64, th=1, tw=1, tc=2, unroll=0, lds=1, ks=1, mfma=0, vec=1))
     assert g == dict(valid=True, grid=56 * 56, threads=64, lds_bytes=4 * (2 * 1172 + 18 + 1152 + 18),
                      acc=1, unroll_eff=1, t0=1, t1=1, red=18, chunks=32)
+    # 16-byte copies need an operand in whole 16-byte rows: chunk rows of
+    # 2 * 9 = 18 weights are not, and a one-column halo is not
+    assert not s.valid(idx_of(s, tk=64, th=1, tw=1, tc=2, unroll=0, lds=1, ks=1, mfma=0, vec=4))
+    # nor without LDS staging
+    assert not s.valid(idx_of(s, tk=4, th=4, tw=32, tc=8, unroll=16, lds=0, ks=2, mfma=0, vec=4))
     # Fewer than 64 outputs: not a full wave.
-    assert not s.valid(idx_of(s, tk=2, th=4, tw=4, tc=1, unroll=0, lds=0, ks=1, mfma=0))
+    assert not s.valid(idx_of(s, tk=2, th=4, tw=4, tc=1, unroll=0, lds=0, ks=1, mfma=0, vec=1))
     # MFMA reduction padded to a multiple of 16: 4 channels x 9 taps = 36 -> 48;
     # 16 columns wide on an image of 56 (a multiple of 4): aligned halo layout,
     # rows of 18 + 3 -> 24 floats; 16 chunks -> two buffers of
     # 32*52 + 4*6*24 + 1 = 2241 -> 2244 floats.
-    g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1))
+    g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1, vec=4))
     assert g["red"] == 48 and g["lds_bytes"] == 4 * (2 * 2244 + 48 + 1664 + 576)
+    # with 4-byte copies the rows keep exactly the tile's 18 input columns:
+    # 32*52 + 4*6*18 + 1 = 2097 -> 2100 floats per buffer
+    g = s.geometry(idx_of(s, tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1, vec=1))
+    assert g["lds_bytes"] == 4 * (2 * 2100 + 48 + 1664 + 432)
     # acc budget: 64 channels x 4 pixels per thread (1024 px / 256) = 256 > 64.
-    assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0))["valid"]
+    assert not s.geometry(idx_of(s, tk=64, th=32, tw=32, tc=1, unroll=0, lds=0, ks=1, mfma=0,
+                                 vec=1))["valid"]
     # MFMA needs >= 16 channels and >= 16 pixels (one 16x16 block per wave).
-    assert not s.valid(idx_of(s, tk=8, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
-    assert not s.valid(idx_of(s, tk=16, th=2, tw=4, tc=4, unroll=0, lds=0, ks=1, mfma=1))
-    assert s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1))
+    assert not s.valid(idx_of(s, tk=8, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1, vec=1))
+    assert not s.valid(idx_of(s, tk=16, th=2, tw=4, tc=4, unroll=0, lds=0, ks=1, mfma=1, vec=1))
+    assert s.valid(idx_of(s, tk=16, th=4, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1, vec=1))
     # LDS limit: 64-channel chunk of a 34-row halo in the aligned layout (rows
     # of 34 + 3 -> 40 floats) does not fit (one chunk, one buffer of
     # 16*576 + 64*34*40 + 1 -> 96260 floats).
-    g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0))
+    g = s.geometry(idx_of(s, tk=16, th=32, tw=32, tc=64, unroll=0, lds=1, ks=1, mfma=0, vec=4))
     assert g["lds_bytes"] == 4 * (96260 + 576 + 9216 + 87040) and not g["valid"]
     # split finer than the chunk count.
-    assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0))
+    assert not s.valid(idx_of(s, tk=16, th=8, tw=8, tc=64, unroll=0, lds=0, ks=2, mfma=0, vec=1))
+    # register budgets of the compiled kernels: one 16-channel block x 32
+    # pixel blocks per wave (2048 pixels over four waves, on VGG-16 layer 2)
+    # needs two operand sets of 4 * 33 floats = 264 > 192; 2 x 16 blocks fit
+    v = sp.Space(sp.OP_CONV, (16, 64, 224, 224, 64, 3, 3, 1, 1))
+    assert not v.valid(idx_of(v, tk=16, th=64, tw=32, tc=4, unroll=0, lds=1, ks=1, mfma=1, vec=4))
+    g = v.geometry(idx_of(v, tk=32, th=64, tw=16, tc=4, unroll=0, lds=1, ks=1, mfma=1, vec=4))
+    assert g["valid"] and (g["t0"], g["t1"]) == (2, 16)
+    # a third operand set (unroll 64 over 32 blocks -> u = 2, depth 1) is not
+    # reachable there; depth 2 needs 3 * 4 * (tkb + npb) <= 96
+    g = v.geometry(idx_of(v, tk=64, th=8, tw=16, tc=4, unroll=64, lds=1, ks=1, mfma=1, vec=4))
+    assert (g["t0"], g["t1"], g["unroll_eff"]) == (4, 2, 2) and g["valid"]
+    # 64 accumulators (256 pixels, one per thread, x 64 channels) on the
+    # global path with an 8-fold unroll (512 / 64)
+    g = s.geometry(idx_of(s, tk=64, th=16, tw=16, tc=8, unroll=512, lds=0, ks=1, mfma=0, vec=1))
+    assert g["acc"] == 64 and g["unroll_eff"] == 8 and not g["valid"]
+    assert s.valid(idx_of(s, tk=64, th=16, tw=16, tc=8, unroll=64, lds=0, ks=1, mfma=0, vec=1))
 
 
 def test_conv_mfma_small_tile_geometry():
@@ -123,48 +156,63 @@ def test_conv_mfma_small_tile_geometry():
     # ceil((16*148 + 16*36 + 1) / 4) * 4 = 2948 floats, then the 144-entry table
     # and the staging sources (2368 + 576).
     s = sp.Space(sp.OP_CONV, (1, 512, 7, 7, 512, 3, 3, 1, 1))
-    g = s.geometry(idx_of(s, tk=16, th=4, tw=4, tc=16, unroll=64, lds=1, ks=8, mfma=1))
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=4, tc=16, unroll=64, lds=1, ks=8, mfma=1, vec=4))
     assert g == dict(valid=True, grid=8 * 32 * 2 * 2, threads=64,
                      lds_bytes=4 * (2 * 2948 + 144 + 2368 + 576),
-                     acc=4, unroll_eff=16, t0=1, t1=1, red=144, chunks=32)
+                     acc=4, unroll_eff=3, t0=1, t1=1, red=144, chunks=32)
     # two 16-channel blocks on the one wave
-    g = s.geometry(idx_of(s, tk=32, th=4, tw=4, tc=16, unroll=0, lds=0, ks=4, mfma=1))
+    g = s.geometry(idx_of(s, tk=32, th=4, tw=4, tc=16, unroll=0, lds=0, ks=4, mfma=1, vec=1))
     assert g["valid"] and g["threads"] == 64 and g["t0"] == 2 and g["t1"] == 1
     # 8 pixels: less than one 16-pixel block
-    assert not s.valid(idx_of(s, tk=32, th=4, tw=2, tc=16, unroll=0, lds=0, ks=4, mfma=1))
+    assert not s.valid(idx_of(s, tk=32, th=4, tw=2, tc=16, unroll=0, lds=0, ks=4, mfma=1, vec=1))
     # 32 pixels: two waves, one block each.
     c = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
-    g = c.geometry(idx_of(c, tk=16, th=4, tw=8, tc=16, unroll=0, lds=1, ks=1, mfma=1))
+    g = c.geometry(idx_of(c, tk=16, th=4, tw=8, tc=16, unroll=0, lds=1, ks=1, mfma=1, vec=4))
     assert g["valid"] and g["threads"] == 128 and g["t1"] == 1
 
 
 def test_matmul_geometry_hand_computed():
     m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
-    g = m.geometry(idx_of(m, bm=64, bn=64, bk=16, unroll=64, dbuf=1, mfma=1, ks=1))
+    g = m.geometry(idx_of(m, bm=64, bn=64, bk=16, unroll=64, dbuf=1, mfma=1, ks=1, vec=4))
     # dbuf: three stages of 8 KiB fit.
     assert g == dict(valid=True, grid=256, threads=256, lds_bytes=3 * (64 * 16 + 16 * 64) * 4,
                      acc=16, unroll_eff=8, t0=32, t1=32, red=2, chunks=64)
-    g = m.geometry(idx_of(m, bm=32, bn=128, bk=32, unroll=16, dbuf=0, mfma=1, ks=4))
+    g = m.geometry(idx_of(m, bm=32, bn=128, bk=32, unroll=16, dbuf=0, mfma=1, ks=4, vec=4))
     # wave tile 16x64 -> 16x16x4 blocks: 1*4, acc 16; trip 8, 8*4 > 16 -> 16//4 = 4.
     # ks 4: two wave groups (512 threads) x two workgroup splits; LDS holds the
     # larger of one stage (5120 floats) and the 32x128 partial tile (4096).
     assert g == dict(valid=True, grid=32 * 8 * 2, threads=512, lds_bytes=(32 * 32 + 32 * 128) * 4,
                      acc=16, unroll_eff=4, t0=16, t1=64, red=4, chunks=32)
     # dbuf with 2 x 64 KiB stages: three do not fit, two do.
-    g = m.geometry(idx_of(m, bm=128, bn=128, bk=64, unroll=0, dbuf=1, mfma=1, ks=1))
+    g = m.geometry(idx_of(m, bm=128, bn=128, bk=64, unroll=0, dbuf=1, mfma=1, ks=1, vec=4))
     assert g["valid"] and g["lds_bytes"] == 2 * (128 * 64 + 64 * 128) * 4
     # ks 2 with a K-tile of 4 steps stays a two-workgroup split of 256 threads.
-    g = m.geometry(idx_of(m, bm=64, bn=64, bk=4, unroll=0, dbuf=0, mfma=1, ks=2))
+    g = m.geometry(idx_of(m, bm=64, bn=64, bk=4, unroll=0, dbuf=0, mfma=1, ks=2, vec=4))
     assert g["threads"] == 256 and g["grid"] == 16 * 16 * 2
     # ks 2 with 256x256 tiles: the partial tile (256 KiB) does not fit in LDS.
-    assert not m.valid(idx_of(m, bm=256, bn=256, bk=8, unroll=0, dbuf=0, mfma=1, ks=2))
-    g = m.geometry(idx_of(m, bm=128, bn=64, bk=8, unroll=512, dbuf=0, mfma=0, ks=1))
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=8, unroll=0, dbuf=0, mfma=1, ks=2, vec=4))
+    g = m.geometry(idx_of(m, bm=128, bn=64, bk=8, unroll=512, dbuf=0, mfma=0, ks=1, vec=4))
     assert g == dict(valid=True, grid=8 * 16, threads=256, lds_bytes=(128 * 8 + 8 * 64) * 4,
                      acc=32, unroll_eff=8, t0=8, t1=4, red=1, chunks=128)
-    assert not m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=0, ks=1))  # acc 256
-    assert m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=1, ks=1))      # AGPRs
-    assert not m.valid(idx_of(m, bm=256, bn=256, bk=64, unroll=0, dbuf=1, mfma=1, ks=1))  # LDS
-    assert not m.valid(idx_of(m, bm=16, bn=64, bk=8, unroll=0, dbuf=0, mfma=1, ks=1))    # MFMA min
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=0, ks=1, vec=4))  # acc 256
+    assert m.valid(idx_of(m, bm=256, bn=256, bk=4, unroll=0, dbuf=0, mfma=1, ks=1, vec=4))      # AGPRs
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=64, unroll=0, dbuf=1, mfma=1, ks=1, vec=4))  # LDS
+    assert not m.valid(idx_of(m, bm=16, bn=64, bk=8, unroll=0, dbuf=0, mfma=1, ks=1, vec=4))    # MFMA min
+    # register budgets of the compiled kernels: two wave groups (ks 2, bk >= 8)
+    # hold at most 64 accumulators (64x128 wave tile: 128)
+    assert not m.valid(idx_of(m, bm=128, bn=256, bk=8, unroll=0, dbuf=0, mfma=1, ks=2, vec=4))
+    assert m.valid(idx_of(m, bm=128, bn=256, bk=8, unroll=0, dbuf=0, mfma=1, ks=1, vec=4))
+    # 128x128 wave tile, 16-deep K-tile unrolled 8 times (trip 8 * 16 blocks <= 512), one stage
+    assert not m.valid(idx_of(m, bm=256, bn=256, bk=16, unroll=512, dbuf=0, mfma=1, ks=1, vec=4))
+    assert m.valid(idx_of(m, bm=256, bn=256, bk=16, unroll=512, dbuf=1, mfma=1, ks=1, vec=4))
+    # VALU 1x16 per thread, 32-deep K-tile fully unrolled (16 * 32 <= 512), staged
+    # through registers: (1 + 16) * 32 = 544 > 512
+    assert not m.valid(idx_of(m, bm=16, bn=256, bk=32, unroll=512, dbuf=1, mfma=0, ks=1, vec=4))
+    assert m.valid(idx_of(m, bm=16, bn=256, bk=32, unroll=512, dbuf=0, mfma=0, ks=1, vec=4))
+    # 16-byte loads need K or N in whole 16-byte groups
+    o = sp.Space(sp.OP_MATMUL, (33, 45, 7))
+    assert not o.valid(idx_of(o, bm=16, bn=16, bk=4, unroll=0, dbuf=0, mfma=0, ks=1, vec=4))
+    assert o.valid(idx_of(o, bm=16, bn=16, bk=4, unroll=0, dbuf=0, mfma=0, ks=1, vec=1))
 
 
 @pytest.mark.parametrize("op,shape", [

@@ -56,11 +56,11 @@ def run_both(torch, L, op, sh, knobs, kind="uniform"):
 
 
 CONV_BIG = ((1, 64, 56, 56, 64, 3, 3, 1, 1),
-            dict(tk=16, th=4, tw=32, tc=32, unroll=16, lds=1, ks=2, mfma=1))
+            dict(tk=16, th=4, tw=32, tc=32, unroll=16, lds=1, ks=2, mfma=1, vec=4))
 CONV_SMALL = ((1, 48, 13, 11, 40, 3, 3, 1, 1),
-              dict(tk=16, th=4, tw=8, tc=4, unroll=0, lds=1, ks=4, mfma=1))
-MM_BIG = ((256, 512, 1024), dict(bm=64, bn=64, bk=32, unroll=16, dbuf=1, mfma=1, ks=4))
-MM_SMALL = ((33, 45, 70), dict(bm=16, bn=16, bk=8, unroll=0, dbuf=0, mfma=0, ks=8))
+              dict(tk=16, th=4, tw=8, tc=4, unroll=0, lds=1, ks=4, mfma=1, vec=4))
+MM_BIG = ((256, 512, 1024), dict(bm=64, bn=64, bk=32, unroll=16, dbuf=1, mfma=1, ks=4, vec=4))
+MM_SMALL = ((33, 45, 70), dict(bm=16, bn=16, bk=8, unroll=0, dbuf=0, mfma=0, ks=8, vec=1))
 
 
 def test_two_calls_conv_then_smaller(env):
@@ -78,7 +78,7 @@ def test_two_calls_matmul_then_smaller(env):
 def test_unsplit_schedule_needs_no_scratch(env):
     torch, L = env
     run_both(torch, L, L.DS_OP_CONV2D_NCHW, (1, 3, 30, 30, 64, 7, 7, 2, 3),
-             dict(tk=16, th=4, tw=8, tc=1, unroll=0, lds=1, ks=1, mfma=1))
+             dict(tk=16, th=4, tw=8, tc=1, unroll=0, lds=1, ks=1, mfma=1, vec=1))
 
 
 def test_partials_beyond_the_array_are_refused(env):
@@ -86,7 +86,7 @@ def test_partials_beyond_the_array_are_refused(env):
     # VGG-16 layer 2 at batch 16: 16*64*224*224 outputs, two splits -> 102.8M floats
     sh = (16, 64, 224, 224, 64, 3, 3, 1, 1)
     space = L.Space(L.DS_OP_CONV2D_NCHW, sh)
-    s = space.sched_of(tk=64, th=4, tw=16, tc=16, unroll=0, lds=1, ks=2, mfma=1)
+    s = space.sched_of(tk=64, th=4, tw=16, tc=16, unroll=0, lds=1, ks=2, mfma=1, vec=4)
     assert space.valid(s.index())
     P, Q = osp.conv_out(sh)
     assert 2 * sh[0] * sh[4] * P * Q > L.DS_NOALLOC_MAX_FLOATS
