@@ -69,10 +69,14 @@ typedef struct ds_space ds_space;
  * sched_space_create -- the kernel search space of one kernel family at one
  * shape (Definition 1).  conv2d axes, in order: tk, th, tw, tc (powers of two
  * 1..64 kept if <= K, P, Q, C), unroll {0,16,64,512}, lds {0,1}, ks
- * {1,2,4,8} (kept if <= C), mfma {0,1}.  matmul axes: bm, bn
- * {16,...,256} (kept if <= M, N), bk {4,...,64} (kept if <= K), unroll,
- * dbuf {0,1}, mfma {0,1}, ks {1,2,4,8} (kept if <= K).  The smallest value of
- * a clipped axis is always kept.  Accepted shapes: conv N >= 0 (0 is the empty
+ * {1,2,4,8} (kept if <= C), mfma {0,1}, vec {1,4} (floats per lane of the
+ * global -> LDS copies).  matmul axes: bm, bn {16,...,256} (kept if <= M, N),
+ * bk {4,...,64} (kept if <= K), unroll, dbuf {0,1}, mfma {0,1}, ks {1,2,4,8}
+ * (kept if <= K), vec {1,4} (floats per lane of the operand loads).  The
+ * smallest value of a clipped axis is always kept.  A point is valid when its
+ * kernel fits the hardware (threads, LDS, workgroups) and the register budget
+ * of its compiled instance (no spill), and, for vec 4, an operand can move 16
+ * bytes per lane.  Accepted shapes: conv N >= 0 (0 is the empty
  * batch), C,H,W,K,R,S,stride >= 1, pad >= 0, at least one output position;
  * matmul M >= 0, N,K >= 1.  *out receives a new space (free it with
  * sched_space_destroy).  Errors: DS_EINVAL, DS_EUNSUPPORTED, DS_ENOMEM.
@@ -126,7 +130,8 @@ typedef struct {
     int64_t grid;         /* number of workgroups (1-D) */
     int32_t lds_bytes;    /* dynamic LDS per workgroup */
     int32_t acc;          /* fp32 accumulators per lane */
-    int32_t unroll_eff;   /* unroll factor of the reduction loop */
+    int32_t unroll_eff;   /* unroll factor of the reduction loop (conv MFMA: the
+                             number of 16-step groups read ahead, 1..3) */
     int32_t t0, t1;       /* conv VALU: channels, pixels per thread; conv MFMA:
                              16-channel blocks, 16-pixel blocks per wave;
                              matmul VALU: rows, cols per thread; matmul MFMA:
