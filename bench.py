@@ -82,16 +82,14 @@ def workload_tasks(name, layers=""):
             for i in parse_layers(layers, len(tasks))], "he"
 
 
-def kernel_name(op, knobs, geom):
+FAMILY_NAME = {1: "conv_valu", 2: "conv_mfma", 3: "mm_valu", 4: "mm_mfma", 5: "conv_mfma2"}
+
+
+def kernel_name(space, idx):
     """Template instance the schedule selects (as rocprofv3 lists it)."""
-    if op == 2:
-        if knobs["mfma"]:
-            return (f"mm_mfma<{geom['t0']}, {geom['t1']}, {knobs['bk']}, {geom['unroll_eff']}, "
-                    f"{knobs['dbuf']}, {geom['threads'] // 256}>")
-        return (f"mm_valu<{geom['t0']}, {geom['t1']}, {knobs['bk']}, {geom['unroll_eff']}, "
-                f"{knobs['dbuf']}>")
-    fam = "conv_mfma" if knobs["mfma"] else "conv_valu"
-    return f"{fam}<{geom['t0']}, {geom['t1']}, {geom['unroll_eff']}, {knobs['lds']}>"
+    info = space.kernel_info(idx)
+    args = ", ".join(str(v) for v in info["params"][: info["nparams"]])
+    return f"{FAMILY_NAME[info['family']]}<{args}>"
 
 
 def roof(flops, nbytes, seconds):
@@ -169,7 +167,7 @@ class Workload:
             task.update(best=res.best, res=res, meas=m,
                         knobs=task["space"].knobs(res.best),
                         geom=task["space"].geometry(res.best.index()))
-            task["kernel"] = kernel_name(task["op"], task["knobs"], task["geom"])
+            task["kernel"] = kernel_name(task["space"], res.best.index())
             log(f"tuned {self.name}/{task['name']}: {task['knobs']} {m.median_ms * 1e3:.2f} us "
                 f"({task['flops'] / (m.median_ms * 1e-3) / 1e9:.0f} GFLOP/s), explored "
                 f"{res.n_explore_measured}, droplet {res.n_droplet_measured}, "

@@ -19,7 +19,9 @@ conv2d (op 1), shape (N, C, H, W, K, R, S, stride, pad), axes in order
     unroll in {0, 16, 64, 512}: maximum unrolled steps of the reduction loop;
     lds in {0, 1}: stage input and weight tiles in LDS;
     ks in {1, 2, 4, 8}: reduction split over C across workgroups (kept if <= C);
-    mfma in {0, 1}: contract on fp32 MFMA (implicit GEMM) instead of VALU FMA;
+    mfma in {0, 1, 2}: contract on VALU FMA (0) or fp32 MFMA (implicit GEMM):
+        1 steps through 16-step groups of the (c, r, s) reduction, 2 through
+        (tap, channel quad) steps (a second MFMA sketch, LDS staging only);
     vec in {1, 4}: floats per lane of the global -> LDS copies (4 or 16 bytes).
 
 matmul (op 2), shape (M, N, K), axes in order
@@ -201,7 +203,7 @@ class Space(Lattice):
             P, Q = conv_out(shape)
             values = [
                 _clip(POW2_64, K), _clip(POW2_64, P), _clip(POW2_64, Q), _clip(POW2_64, C),
-                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1], list(VEC),
+                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1, 2], list(VEC),
             ]
             names = CONV_AXES
         else:
@@ -221,6 +223,8 @@ class Space(Lattice):
 
 
 def conv_geometry(shape, v):
+    if v["mfma"] == 2:
+        return conv_quad_geometry(shape, v)
     N, C, H, W, K, R, S, st, pd = shape
     P, Q = conv_out(shape)
     tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
@@ -299,6 +303,74 @@ def conv_geometry(shape, v):
              and grid <= GRID_LIMIT)
     return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=acc,
                 unroll_eff=uf, t0=t0, t1=t1, red=red, chunks=chunks)
+
+
+def conv_quad_geometry(shape, v):
+    """mfma = 2: implicit GEMM whose k-steps each take one channel quad (four
+    consecutive input channels) at one tap (r, s), over LDS-staged weights and
+    input halo.  Waves split the tile's pixels as for mfma = 1 (16x16 blocks,
+    up to four pixel waves); the unroll knob gives the depth D (3 from 16
+    unrolled steps, 2 from 4, else 1) and a step takes U = 2^(D-1) quads.  A
+    reduction split ks first goes to KG wave groups of one workgroup (the
+    largest of 4, 2, 1 not above ks whose U-blocks of quads divide the chunk's
+    quads and that keeps 1024 threads), the rest across workgroups.
+
+    LDS per buffer: tk weight rows of wrow floats (the smallest 4 * odd >=
+    4 * quads * R * S) and 4 * quads halo channels of cs floats (the smallest
+    >= hs * ws that is 16 mod 32); two buffers when a workgroup walks more than
+    one chunk; the wave groups' partial tiles reuse it.  Validity adds: at
+    least one 16x16 block, chunks of whole channel quads (tc >= 4, or tc = 1
+    standing for all channels of an image with fewer than four), LDS staging,
+    the register budget of the compiled instances (at most 32, 16, 4 blocks
+    per wave and 20, 12, 8 channel plus pixel blocks for KG = 1, 2, 4), and
+    at most 12 copy units per thread per kind
+    for a full chunk (4-byte units, or 16-byte ones where rows allow: vec).
+    """
+    N, C, H, W, K, R, S, st, pd = shape
+    P, Q = conv_out(shape)
+    tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
+    npx = th * tw
+    waves = min(4, max(1, npx // 16))
+    tkb, npb = max(1, tk // 16), max(1, npx // (16 * waves))
+    blocks = tkb * npb
+    uf = 1 if v["unroll"] == 0 else min(16, _pow2floor(max(1, v["unroll"] // blocks)))
+    depth = 3 if uf >= 16 else (2 if uf >= 4 else 1)
+    quads_per_step = 2 ** (depth - 1)
+    chan = C if C < 4 else tc                  # real channels of a full chunk
+    quads = _cdiv(chan, 4)
+    ok = tk >= 16 and npx >= 16 and (tc >= 4 or (C < 4 and tc == 1))
+    kg = min(v["ks"], 4)
+    while kg > 1 and (quads % (kg * quads_per_step) or 64 * waves * kg > THREADS_LIMIT):
+        kg //= 2
+    ksw = v["ks"] // kg
+    ok = ok and 4 * blocks <= 128 and quads % (kg * quads_per_step) == 0
+    ok = ok and blocks <= {1: 32, 2: 16, 4: 4}[kg] and tkb + npb <= {1: 20, 2: 12, 4: 8}[kg]
+    chunks = _cdiv(C, chan)
+    cps = _cdiv(chunks, ksw)
+    ok = ok and ksw <= chunks
+    hs = (th - 1) * st + R
+    halo16 = v["vec"] == 4 and W % 4 == 0 and tw * st >= 16
+    ws = _cdiv((tw - 1) * st + S + 3, 4) * 4 if halo16 else (tw - 1) * st + S
+    cs = hs * ws
+    while cs % 32 != 16:
+        cs += 1
+    half_row = quads * R * S                   # weight row floats / 4
+    wrow = 4 * (half_row if half_row % 2 else half_row + 1)
+    w16 = v["vec"] == 4 and (C * R * S) % 4 == 0 and (chan * R * S) % 4 == 0
+    ok = ok and (v["vec"] == 1 or w16 or halo16)
+    threads = 64 * waves * kg
+    units_w = tk * wrow // 4 if w16 else tk * wrow
+    units_h = quads * cs if halo16 else 4 * quads * cs
+    per_thread = max(_cdiv(units_w, threads), _cdiv(units_h, threads))
+    ok = ok and (C < 4 or per_thread <= 12)
+    nbuf = 2 if cps > 1 else 1
+    buf = tk * wrow + 4 * quads * cs
+    lds = max(4 * nbuf * buf, 16 * (kg - 1) * waves * 64 * blocks)
+    grid = N * ksw * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)
+    valid = (ok and v["lds"] == 1 and lds <= LDS_LIMIT and threads <= THREADS_LIMIT
+             and grid <= GRID_LIMIT)
+    return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=4 * blocks,
+                unroll_eff=depth, t0=tkb, t1=npb, red=4 * quads * R * S, chunks=chunks)
 
 
 def matmul_geometry(shape, v):

@@ -1,6 +1,7 @@
 // Internal declarations shared by the library's translation units.
 #pragma once
 
+#include <algorithm>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -122,6 +123,149 @@ struct MatmulArgs {
     int gm;               // tile rows per group of the XCD tile order (mm_group_rows)
 };
 
+// Arguments of the channel-quad MFMA conv (conv_mfma2, mfma = 2).  A
+// workgroup stages, per reduction chunk of tc channels, the weights of its tk
+// output channels ([kl][c_l*R*S + r*S + s], rows wrow floats apart) and the
+// input halo of its tile ([c_l][hy][hx], channels cs floats apart) in LDS; one
+// MFMA k-step takes four consecutive channels (a "quad") at one tap (r, s), so
+// both operands are read at a uniform offset from a per-lane base.
+struct Conv2Args {
+    const float *x;
+    const float *w;
+    float *y;
+    float *part;          // ksw > 1: split z writes its partial output at part + z * N*K*P*Q
+    int N, C, H, W, K, R, S, st, pd, P, Q;
+    int tk, th, tw, tc;   // tc: real channels of a full chunk (C when C < 4)
+    int tiles_k, tiles_p, tiles_q, ksw;   // ksw: reduction splits across workgroups
+    int chunks, cps;      // reduction chunks, chunks per split
+    int t4;               // channel quads per chunk (channel slots / 4)
+    int hs, ws, cs;       // halo rows, halo row stride, halo channel stride (floats)
+    int wrow;             // weight row stride (floats, 4 * odd)
+    int npx, ltw, wpx, lwpx;   // tile pixels, log2(tw), pixel waves and log2
+    int bufw, buf;        // floats of the weight part of a buffer, of a whole buffer
+    int nbuf;             // LDS buffers (2 when a workgroup walks more than one chunk)
+    int hal;              // aligned halo layout: rows start at the 16-byte boundary at
+                          //    or before the tile's first column (W % 4 == 0, tw*st >= 16)
+    int vw, vh;           // 16-byte copies of weight / halo units (else 4-byte)
+    int nw4, nh4;         // copy units of a chunk (weights, halo)
+    int ncopy;            // copy units per thread per kind
+    int regs;             // ncopy <= kConv2RegCopies: a full chunk's sources stay in registers
+    int wr_u, hc_u, hr_u; // copy units per weight row, halo channel, halo row
+    int w_dk, w_dc;       // blockDim in (weight row, unit) mixed radix
+    int h_dc, h_dr;       // blockDim in (halo channel, unit) mixed radix
+    FastDiv f_wru, f_hcu, f_hru, f_rs, f_s, f_tk, f_tq, f_tp, f_ksw;
+};
+
+// Launch shape of a conv_mfma2 point.
+struct Conv2Shape {
+    bool valid = false;
+    int tkb = 0, npb = 0, u = 1, kg = 1;   // template parameters
+    int threads = 0;
+    int64_t grid = 0;
+    int64_t lds = 0;
+    int red = 0;                          // channel slots x taps of one chunk
+};
+
+constexpr int kConv2RegCopies = 12;       // copy units per thread held in registers
+
+// Register budget of the compiled conv_mfma2 instances (no spill; launch bound
+// 256 * KG): TKB x NPB blocks per wave and TKB + NPB operand floats per quad.
+constexpr bool conv2_regs_ok(int tkb, int npb, int kg) {
+    return tkb * npb <= (kg == 4 ? 4 : kg == 2 ? 16 : 32) &&
+           tkb + npb <= (kg == 4 ? 8 : kg == 2 ? 12 : 20);
+}
+
+// Copy units of conv_mfma2 for its copy widths (vw, vh) and thread count.
+inline void conv2_units(Conv2Args &a, int threads) {
+    const int tc4 = 4 * a.t4;
+    a.nw4 = a.vw ? a.bufw / 4 : a.bufw;
+    a.nh4 = int(a.vh ? int64_t(tc4) * a.cs / 4 : std::min<int64_t>(int64_t(tc4) * a.cs, INT32_MAX));
+    a.ncopy = std::max((a.nw4 + threads - 1) / threads, (a.nh4 + threads - 1) / threads);
+    a.regs = a.ncopy <= kConv2RegCopies;
+    a.wr_u = a.vw ? a.wrow / 4 : a.wrow;
+    a.hc_u = a.vh ? a.cs / 4 : a.cs;
+    a.hr_u = a.vh ? a.ws / 4 : a.ws;
+    a.w_dk = threads / a.wr_u; a.w_dc = threads % a.wr_u;
+    a.h_dc = threads / a.hc_u; a.h_dr = threads % a.hc_u;
+    a.f_wru = make_fastdiv(a.wr_u); a.f_hcu = make_fastdiv(a.hc_u); a.f_hru = make_fastdiv(a.hr_u);
+}
+
+// Set-up of conv_mfma2 for shape sh and knob values (depth D = 1..3 from the
+// unroll knob; the k-steps unrolled per loop step are U = 2^(D-1) quads).
+// The in-workgroup reduction split KG is the largest of 4, 2, 1 not above ks
+// that divides the quads of a chunk into whole U-blocks and fits 1024
+// threads; the rest of ks splits across workgroups.  Fills a (buffers aside)
+// and returns the shape with its validity: a tile of at least one 16x16
+// block, chunks of whole channel quads (tc >= 4, or for fewer than four
+// image channels tc = 1 standing for all of them), the register budget of
+// the compiled instances (no spill), the copy units a thread holds, LDS.
+inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc, int depth, int ks,
+                              int vec, Conv2Args &a) {
+    Conv2Shape g;
+    a = Conv2Args();
+    a.N = int(sh[0]); a.C = int(sh[1]); a.H = int(sh[2]); a.W = int(sh[3]); a.K = int(sh[4]);
+    a.R = int(sh[5]); a.S = int(sh[6]); a.st = int(sh[7]); a.pd = int(sh[8]);
+    a.P = int(conv_out_dim(sh[2], sh[5], sh[7], sh[8]));
+    a.Q = int(conv_out_dim(sh[3], sh[6], sh[7], sh[8]));
+    a.tk = tk; a.th = th; a.tw = tw;
+    const int RS = a.R * a.S;
+    bool ok = tk >= 16 && th * tw >= 16 && (tc >= 4 || (a.C < 4 && tc == 1));
+    a.tc = a.C < 4 ? a.C : tc;
+    const int tc4 = (a.tc + 3) / 4 * 4;
+    a.t4 = tc4 / 4;
+    a.npx = th * tw;
+    a.wpx = std::min(4, std::max(1, a.npx / 16));
+    a.lwpx = a.wpx >= 4 ? 2 : a.wpx - 1;
+    int l = 0;
+    while ((1 << l) < tw) ++l;
+    a.ltw = l;
+    g.tkb = std::max(1, tk / 16);
+    g.npb = std::max(1, a.npx / (16 * a.wpx));
+    g.u = 1 << (depth - 1);
+    int kg = std::min(ks, 4);
+    while (kg > 1 && (a.t4 % (kg * g.u) != 0 || 64 * a.wpx * kg > 1024)) kg /= 2;
+    g.kg = kg;
+    a.ksw = ks / kg;
+    const int body = g.tkb * g.npb;
+    ok = ok && 4 * body <= 128 && a.t4 % (kg * g.u) == 0 && conv2_regs_ok(g.tkb, g.npb, kg);
+    a.chunks = int((a.C + a.tc - 1) / a.tc);
+    a.cps = (a.chunks + a.ksw - 1) / a.ksw;
+    ok = ok && a.ksw <= a.chunks;
+    a.hs = (th - 1) * a.st + a.R;
+    const bool halo16 = vec == 4 && a.W % 4 == 0 && int64_t(tw) * a.st >= 16;
+    a.ws = halo16 ? int(((int64_t(tw - 1) * a.st + a.S + 3 + 3) / 4) * 4) : (tw - 1) * a.st + a.S;
+    int64_t cs = int64_t(a.hs) * a.ws;
+    cs += ((16 - cs % 32) + 32) % 32;                 // cs = 16 mod 32: the four lane groups'
+    a.cs = int(std::min<int64_t>(cs, INT32_MAX));     // channels fall on disjoint banks
+    int64_t r4 = (int64_t(tc4) * RS + 3) / 4;
+    if (r4 % 2 == 0) ++r4;                            // rows 4*odd floats apart: the 16 rows of
+    a.wrow = int(std::min<int64_t>(4 * r4, INT32_MAX));   // a block fall on disjoint banks
+    a.vw = vec == 4 && (int64_t(a.C) * RS) % 4 == 0 && (int64_t(a.tc) * RS) % 4 == 0;
+    a.hal = halo16;
+    a.vh = halo16;
+    ok = ok && (vec == 1 || a.vw || a.vh);
+    a.bufw = int(std::min<int64_t>(int64_t(tk) * a.wrow, INT32_MAX));
+    const int64_t buf = int64_t(tk) * a.wrow + int64_t(tc4) * a.cs;
+    a.buf = int(std::min<int64_t>(buf, INT32_MAX));
+    a.nbuf = a.cps > 1 ? 2 : 1;
+    g.threads = 64 * a.wpx * kg;
+    conv2_units(a, g.threads);
+    // a full chunk's copy units are held in registers (chunks with channel
+    // slots past C, C < 4, compute theirs as they go)
+    ok = ok && (a.C < 4 || a.regs);
+    a.tiles_k = int((a.K + tk - 1) / tk);
+    a.tiles_p = int((a.P + th - 1) / th);
+    a.tiles_q = int((a.Q + tw - 1) / tw);
+    a.f_rs = make_fastdiv(RS); a.f_s = make_fastdiv(a.S);
+    a.f_tk = make_fastdiv(a.tiles_k); a.f_tq = make_fastdiv(a.tiles_q);
+    a.f_tp = make_fastdiv(a.tiles_p); a.f_ksw = make_fastdiv(a.ksw);
+    g.lds = std::max<int64_t>(4 * int64_t(a.nbuf) * buf, int64_t(16) * (kg - 1) * a.wpx * 64 * body);
+    g.grid = int64_t(a.N) * a.ksw * a.tiles_k * a.tiles_p * a.tiles_q;
+    g.red = tc4 * RS;
+    g.valid = ok && g.lds <= kLdsLimit && g.threads <= kThreadsLimit && g.grid <= kGridLimit;
+    return g;
+}
+
 // Tile rows per group of the matmul tile order: the power of two (at most
 // tiles_m) that minimises the A rows plus B columns, in elements, touched by
 // the contiguous tile range of one XCD (ties: the smaller), so that range is
@@ -157,6 +301,7 @@ struct Plan {
     int64_t y_elems = 0;
     int op = 0;
     ConvArgs conv{};
+    Conv2Args conv2{};        // family DS_KERNEL_CONV_MFMA2
     MatmulArgs mm{};
 };
 
@@ -169,6 +314,7 @@ int launch_plan(const Plan &plan, hipStream_t stream);
 // Kernel instance lookup (compiled template instances).
 const void *conv_valu_instance(int kpt, int ppt, int uf, int lds);
 const void *conv_mfma_instance(int tkb, int npb, int d, int lds);
+const void *conv_mfma2_instance(int tkb, int npb, int u, int kg);
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf);
 const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf, int kg);
 int count_instances();

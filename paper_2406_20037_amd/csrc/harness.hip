@@ -18,6 +18,7 @@ const Space &space_of(const ds_space *s);
 
 const void *g_conv_valu[kConvValuSlots];
 const void *g_conv_mfma[kConvMfmaSlots];
+const void *g_conv_mfma2[kConvMfma2Slots];
 const void *g_mm_valu[kMmValuSlots];
 const void *g_mm_mfma[kMmMfmaSlots];
 
@@ -428,6 +429,12 @@ const void *conv_mfma_instance(int tkb, int npb, int d, int lds) {
     return g_conv_mfma[((a * 7 + b) * 3 + d - 1) * 2 + lds];
 }
 
+const void *conv_mfma2_instance(int tkb, int npb, int u, int kg) {
+    const int a = log2_exact(tkb), b = log2_exact(npb), c = log2_exact(u), d = log2_exact(kg);
+    if (a < 0 || a > 2 || b < 0 || b > 5 || c < 0 || c > 2 || d < 0 || d > 2) return nullptr;
+    return g_conv_mfma2[((a * 6 + b) * 3 + c) * 3 + d];
+}
+
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf) {
     const int a = log2_exact(rm), b = log2_exact(rn), k = log2_exact(bk) - 2, c = log2_exact(uf);
     if (a < 0 || a > 4 || b < 0 || b > 4 || k < 0 || k > 4 || c < 0 || c > 6 || (dbuf & ~1))
@@ -448,6 +455,7 @@ int count_instances() {
     int n = 0;
     for (auto p : g_conv_valu) n += p != nullptr;
     for (auto p : g_conv_mfma) n += p != nullptr;
+    for (auto p : g_conv_mfma2) n += p != nullptr;
     for (auto p : g_mm_valu) n += p != nullptr;
     for (auto p : g_mm_mfma) n += p != nullptr;
     return n;
@@ -478,7 +486,30 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
     plan.threads = g.threads;
     plan.grid = g.grid;
     plan.lds = g.lds_bytes;
-    if (s->op == DS_OP_CONV2D_NCHW) {
+    if (s->op == DS_OP_CONV2D_NCHW && sp.value(s->idx, 7) == 2) {
+        Conv2Args &a = plan.conv2;
+        const Conv2Shape c = conv2_setup(sp.shape, sp.value(s->idx, 0), sp.value(s->idx, 1),
+                                         sp.value(s->idx, 2), sp.value(s->idx, 3), g.unroll_eff,
+                                         sp.value(s->idx, 6), sp.value(s->idx, 8), a);
+        a.x = x;
+        a.w = w;
+        a.y = y;
+        // 16-byte copies only from 16-byte aligned operands (else 4-byte
+        // copies into the same layout)
+        const int vw0 = a.vw, vh0 = a.vh;
+        if (reinterpret_cast<uintptr_t>(w) % 16 != 0) a.vw = 0;
+        if (reinterpret_cast<uintptr_t>(x) % 16 != 0) a.vh = 0;
+        if (a.vw != vw0 || a.vh != vh0) conv2_units(a, c.threads);
+        plan.func = conv_mfma2_instance(c.tkb, c.npb, c.u, c.kg);
+        plan.family = DS_KERNEL_CONV_MFMA2;
+        plan.nparams = 4;
+        const int pr[4] = {c.tkb, c.npb, c.u, c.kg};
+        std::memcpy(plan.params, pr, sizeof pr);
+        plan.slot = ((log2_exact(c.tkb) * 6 + log2_exact(c.npb)) * 3 + log2_exact(c.u)) * 3 +
+                    log2_exact(c.kg);
+        plan.splits = a.ksw > 1 ? int(cdiv64(a.chunks, a.cps)) : 1;
+        plan.y_elems = int64_t(a.N) * a.K * a.P * a.Q;
+    } else if (s->op == DS_OP_CONV2D_NCHW) {
         ConvArgs &a = plan.conv;
         fill_conv_args(sp, x, w, y, a);
         a.tk = sp.value(s->idx, 0);
@@ -580,12 +611,15 @@ int64_t workspace_elems(const Plan &plan) {
     if (plan.splits <= 1 || plan.y_elems == 0 || plan.grid == 0) return 0;
     // Splits that own no reduction step exit early; the reduce kernel sums only
     // the first plan.splits partial slices.
-    const int ks = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.ks : plan.mm.ks;
+    const int ks = plan.family == DS_KERNEL_CONV_MFMA2 ? plan.conv2.ksw
+                   : plan.op == DS_OP_CONV2D_NCHW      ? plan.conv.ks
+                                                       : plan.mm.ks;
     return int64_t(ks) * plan.y_elems;
 }
 
 void set_workspace(Plan &plan, float *part) {
-    if (plan.op == DS_OP_CONV2D_NCHW) plan.conv.part = part;
+    if (plan.family == DS_KERNEL_CONV_MFMA2) plan.conv2.part = part;
+    else if (plan.op == DS_OP_CONV2D_NCHW) plan.conv.part = part;
     else plan.mm.part = part;
 }
 
@@ -615,15 +649,18 @@ int launch_plan(const Plan &plan, hipStream_t stream) {
     int rc = ensure_lds_attr(plan.func, plan.lds);
     if (rc != DS_OK) return rc;
     void *args[1];
-    if (plan.op == DS_OP_CONV2D_NCHW) args[0] = const_cast<ConvArgs *>(&plan.conv);
+    if (plan.family == DS_KERNEL_CONV_MFMA2) args[0] = const_cast<Conv2Args *>(&plan.conv2);
+    else if (plan.op == DS_OP_CONV2D_NCHW) args[0] = const_cast<ConvArgs *>(&plan.conv);
     else args[0] = const_cast<MatmulArgs *>(&plan.mm);
     if (!hip_ok(hipLaunchKernel(plan.func, dim3(unsigned(plan.grid)), dim3(plan.threads), args,
                                 size_t(plan.lds), stream),
                 "hipLaunchKernel"))
         return DS_EHIP;
     if (plan.splits > 1) {
-        float *y = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.y : plan.mm.C;
-        const float *part = plan.op == DS_OP_CONV2D_NCHW ? plan.conv.part : plan.mm.part;
+        const bool c2 = plan.family == DS_KERNEL_CONV_MFMA2;
+        float *y = c2 ? plan.conv2.y : plan.op == DS_OP_CONV2D_NCHW ? plan.conv.y : plan.mm.C;
+        const float *part = c2 ? plan.conv2.part
+                               : plan.op == DS_OP_CONV2D_NCHW ? plan.conv.part : plan.mm.part;
         const int64_t n4 = cdiv64(plan.y_elems, 4);
         const int64_t blocks = std::min<int64_t>(cdiv64(n4, 256), 4096);
         const void *reduce[] = {nullptr, nullptr,
@@ -1019,10 +1056,14 @@ int sched_kernel_info(const ds_space *space, const ds_sched *s, int with_attrs,
     out->lds_bytes = plan.lds;
     out->splits = plan.splits;
     // FNV-1a over the kernel's argument block (buffer pointers are null here)
-    const unsigned char *b = plan.op == DS_OP_CONV2D_NCHW
+    const unsigned char *b = plan.family == DS_KERNEL_CONV_MFMA2
+                                 ? reinterpret_cast<const unsigned char *>(&plan.conv2)
+                             : plan.op == DS_OP_CONV2D_NCHW
                                  ? reinterpret_cast<const unsigned char *>(&plan.conv)
                                  : reinterpret_cast<const unsigned char *>(&plan.mm);
-    const size_t nb = plan.op == DS_OP_CONV2D_NCHW ? sizeof plan.conv : sizeof plan.mm;
+    const size_t nb = plan.family == DS_KERNEL_CONV_MFMA2 ? sizeof plan.conv2
+                      : plan.op == DS_OP_CONV2D_NCHW     ? sizeof plan.conv
+                                                         : sizeof plan.mm;
     uint64_t h = 1469598103934665603ull;
     for (size_t i = 0; i < nb; ++i) h = (h ^ b[i]) * 1099511628211ull;
     out->args_hash = h;

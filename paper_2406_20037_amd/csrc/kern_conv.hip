@@ -741,9 +741,310 @@ __global__ __launch_bounds__(256) void conv_mfma(ConvArgs a) {
         }
 }
 
+// ---- channel-quad MFMA conv (mfma = 2) -----------------------------------------
+//
+// Implicit GEMM on v_mfma_f32_16x16x4f32 with the reduction ordered by tap:
+// a k-step multiplies one channel quad (lane group g holds channel 4q + g) at
+// one tap (r, s).  Both operands then sit at a uniform offset from a per-lane
+// base -- weight row 16i + li, column (4q + g)*R*S + r*S + s; halo channel
+// 4q + g, row py*st + r, column px*st + s -- so the loop reads them with plain
+// 4-byte LDS reads and needs no offset table.  A step takes U quads at once;
+// the operands of the next step are read while the current one multiplies.
+// KG wave groups split the quads of every chunk (group g takes quads g,
+// g+KG, ...) and meet in LDS at the end, so a reduction split needs no second
+// launch.  Copy sources of a full chunk are the same for every chunk and are
+// computed once per thread; the next chunk's copies are issued right after
+// the chunk barrier, into the other buffer.
+
+namespace q4 {
+
+__device__ __forceinline__ int fdv(int n, FastDiv f) {
+    return int((__umulhi(unsigned(n), f.m) + unsigned(n)) >> f.s);
+}
+
+// Copy unit u * blockDim + tid of a chunk as (weight row, unit in row) and
+// (halo channel, unit in channel), advanced by blockDim units at a time.
+struct Cursor {
+    int kl, wc, hc, hu;
+    __device__ __forceinline__ void start(const Conv2Args &a, int t) {
+        kl = fdv(t, a.f_wru);
+        wc = t - kl * a.wr_u;
+        hc = fdv(t, a.f_hcu);
+        hu = t - hc * a.hc_u;
+    }
+    __device__ __forceinline__ void next(const Conv2Args &a) {
+        wc += a.w_dc;
+        const bool cw = wc >= a.wr_u;
+        wc -= cw ? a.wr_u : 0;
+        kl += a.w_dk + (cw ? 1 : 0);
+        hu += a.h_dr;
+        const bool ch = hu >= a.hc_u;
+        hu -= ch ? a.hc_u : 0;
+        hc += a.h_dc + (ch ? 1 : 0);
+    }
+};
+
+template <int BYTES>
+__device__ __forceinline__ void copy(const char *base, unsigned off, float *dst) {
+    if constexpr (BYTES == 16)
+        __builtin_amdgcn_global_load_lds(DS_GLOBAL(base + off), DS_LOCAL(dst), 16, 0, 0);
+    else
+        __builtin_amdgcn_global_load_lds(DS_GLOBAL(base + off), DS_LOCAL(dst), 4, 0, 0);
+}
+
+}  // namespace q4
+
+template <int TKB, int NPB, int U, int KG>
+__global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
+    extern __shared__ float smem[];
+    using q4::fdv;
+    // tile of this workgroup (tile order: k, q, p, split, image)
+    const int t0 = xcd_tile(blockIdx.x, gridDim.x);
+    const int t1 = fdv(t0, a.f_tk);
+    const int kt = t0 - t1 * a.tiles_k;
+    const int t2 = fdv(t1, a.f_tq);
+    const int qt = t1 - t2 * a.tiles_q;
+    const int t3 = fdv(t2, a.f_tp);
+    const int pt = t2 - t3 * a.tiles_p;
+    const int n = fdv(t3, a.f_ksw);
+    const int z = t3 - n * a.ksw;
+    const int ci0 = z * a.cps, ci1 = min(ci0 + a.cps, a.chunks);
+    if (ci0 >= ci1) return;
+
+    const int tid = threadIdx.x, nthr = blockDim.x;
+    const int lane = tid & 63;
+    const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = wu >> a.lwpx, wp = wu & (a.wpx - 1);
+    const int li = lane & 15, lg = lane >> 4;
+    const int RS = a.R * a.S;
+    const int PQ = a.P * a.Q;
+    const int slot = wu * 64;
+    const int tc4 = 4 * a.t4;
+    const int hy0 = pt * a.th * a.st - a.pd;
+    const int hx0 = a.hal ? (qt * a.tw * a.st - a.pd) & ~3 : qt * a.tw * a.st - a.pd;
+    const int kvalid = a.K - kt * a.tk;
+    const float *wk = a.w + (size_t)kt * a.tk * a.C * RS;
+    const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
+    auto creal_of = [&](int ci) { return min(a.tc, a.C - ci * a.tc); };
+
+    // Copy sources of a full chunk (byte offsets from its weight / image
+    // base, the same for every full chunk): thread t's u-th unit of a kind is
+    // unit u * blockDim + t.  Weight rows past K and the row padding re-read a
+    // valid float (their LDS positions feed only discarded outputs, or are
+    // never read); halo rows of the channel padding read any valid float
+    // (never read); -1: nothing to copy (past the buffer, or outside the
+    // image: left zero).
+    int sw[kConv2RegCopies], sh[kConv2RegCopies];
+    if (a.regs) {
+        q4::Cursor cur;
+        cur.start(a, tid);
+        const int gw = a.vw ? 4 : 1, gh = a.vh ? 4 : 1;
+#pragma unroll
+        for (int u = 0; u < kConv2RegCopies; ++u) {
+            sw[u] = sh[u] = -1;
+            if (u < a.ncopy) {
+                const int kl = min(cur.kl, kvalid - 1);
+                const int col = min(gw * cur.wc, a.tc * RS - gw);
+                sw[u] = cur.kl < a.tk ? 4 * (kl * a.C * RS + col) : -1;
+                const int hy = fdv(cur.hu, a.f_hru);
+                const int hx = gh * (cur.hu - hy * a.hr_u);
+                const int gy = hy0 + hy, gx = hx0 + hx;
+                const bool in = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+                sh[u] = cur.hc >= tc4 ? -1 : hy >= a.hs ? 0 : in ? 4 * ((cur.hc * a.H + gy) * a.W + gx) : -1;
+                cur.next(a);
+            }
+        }
+    }
+    auto issue_full = [&](int ci, int b) {
+        const char *wb = reinterpret_cast<const char *>(wk + (size_t)ci * a.tc * RS);
+        const char *xb = reinterpret_cast<const char *>(xn + (size_t)ci * a.tc * a.H * a.W);
+        float *wt = smem + b * a.buf;
+        float *xs = wt + a.bufw;
+#pragma unroll
+        for (int u = 0; u < kConv2RegCopies; ++u) {
+            if (u >= a.ncopy) break;
+            const int d = u * nthr + slot;
+            if (sw[u] >= 0) {
+                if (a.vw) q4::copy<16>(wb, unsigned(sw[u]), wt + 4 * d);
+                else q4::copy<4>(wb, unsigned(sw[u]), wt + d);
+            }
+            if (sh[u] >= 0) {
+                if (a.vh) q4::copy<16>(xb, unsigned(sh[u]), xs + 4 * d);
+                else q4::copy<4>(xb, unsigned(sh[u]), xs + d);
+            }
+        }
+    };
+    // Units computed as they are issued: a chunk with channel slots past C
+    // (its buffer zeroed first), or every chunk when a thread's units do not
+    // fit its registers (4-byte copies of misaligned operands).
+    auto issue_units = [&](int ci, int b, bool zero) {
+        float *wt = smem + b * a.buf;
+        float *xs = wt + a.bufw;
+        if (zero) {
+            for (int e = tid; e < a.buf / 4; e += nthr)
+                reinterpret_cast<floatx4 *>(wt)[e] = floatx4{0.f, 0.f, 0.f, 0.f};
+            __syncthreads();
+        }
+        const int creal = creal_of(ci);
+        const char *wb = reinterpret_cast<const char *>(wk + (size_t)ci * a.tc * RS);
+        const char *xb = reinterpret_cast<const char *>(xn + (size_t)ci * a.tc * a.H * a.W);
+        const int gw = a.vw ? 4 : 1, gh = a.vh ? 4 : 1;
+        q4::Cursor cur;
+        cur.start(a, tid);
+        for (int u = 0; u < a.ncopy; ++u, cur.next(a)) {
+            const int d = u * nthr + slot;
+            const int col = gw * cur.wc;
+            if (cur.kl < a.tk && cur.kl < kvalid && col < creal * RS) {
+                if (a.vw) q4::copy<16>(wb, unsigned(4 * (cur.kl * a.C * RS + col)), wt + 4 * d);
+                else q4::copy<4>(wb, unsigned(4 * (cur.kl * a.C * RS + col)), wt + d);
+            }
+            const int hy = fdv(cur.hu, a.f_hru);
+            const int hx = gh * (cur.hu - hy * a.hr_u);
+            const int gy = hy0 + hy, gx = hx0 + hx;
+            if (cur.hc < creal && hy < a.hs && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W) {
+                const unsigned o = unsigned(4 * ((cur.hc * a.H + gy) * a.W + gx));
+                if (a.vh) q4::copy<16>(xb, o, xs + 4 * d);
+                else q4::copy<4>(xb, o, xs + d);
+            }
+        }
+    };
+
+    // Halo positions outside the image are never copied: zero every buffer
+    // once when the tile's halo reaches past the image.
+    const bool border = hy0 < 0 || hy0 + a.hs > a.H || hx0 < 0 || hx0 + a.ws > a.W;
+    if (border) {
+        for (int e = tid; e < a.nbuf * a.buf / 4; e += nthr)
+            reinterpret_cast<floatx4 *>(smem)[e] = floatx4{0.f, 0.f, 0.f, 0.f};
+        __syncthreads();
+    }
+    auto issue = [&](int ci, int b) {
+        if (creal_of(ci) < tc4) issue_units(ci, b, true);
+        else if (a.regs) issue_full(ci, b);
+        else issue_units(ci, b, false);
+    };
+    issue(ci0, 0);
+
+    // lane bases (floats) inside a buffer
+    int bb[NPB], oq[NPB];
+    bool pv[NPB];
+    const int shift = a.hal ? (qt * a.tw * a.st - a.pd) & 3 : 0;
+#pragma unroll
+    for (int b = 0; b < NPB; ++b) {
+        const int pix = (wp * NPB + b) * 16 + li;
+        const int py = pix >> a.ltw, px = pix & (a.tw - 1);
+        const int p = pt * a.th + py, q = qt * a.tw + px;
+        pv[b] = pix < a.npx && p < a.P && q < a.Q;
+        bb[b] = a.bufw + lg * a.cs + py * a.st * a.ws + px * a.st + shift;
+        oq[b] = p * a.Q + q;
+    }
+    const int ab = li * a.wrow + lg * RS;
+    const int sa = 4 * KG * RS, sb = 4 * KG * a.cs;   // quad strides of one group
+
+    floatx4 acc[TKB][NPB];
+#pragma unroll
+    for (int i = 0; i < TKB; ++i)
+#pragma unroll
+        for (int b = 0; b < NPB; ++b) acc[i][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // Step t of a group in a chunk: quad block cq = t / RS (quads
+    // (cq*U + u)*KG + g, u < U) at tap rs = t % RS.
+    const int tg = (a.t4 / (KG * U)) * RS;
+    auto offs = [&](int t, int &oa, int &ob) {
+        t = min(t, tg - 1);   // past the last step: re-read it (never multiplied)
+        const int cq = fdv(t, a.f_rs), rs = t - cq * RS;
+        const int r = fdv(rs, a.f_s), s = rs - r * a.S;
+        const int q = 4 * (cq * U * KG + g);
+        oa = q * RS + rs;
+        ob = q * a.cs + r * a.ws + s;
+    };
+    struct Ops {
+        float A[U][TKB];
+        float B[U][NPB];
+    };
+    for (int ci = ci0; ci < ci1; ++ci) {
+        const int bi = (ci - ci0) & 1;
+        chunk_barrier();
+        if (ci + 1 < ci1) issue(ci + 1, bi ^ 1);
+        const float *buf = smem + bi * a.buf;
+        auto load = [&](int t, Ops &o) {
+            int oa, ob;
+            offs(t, oa, ob);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+                for (int i = 0; i < TKB; ++i) o.A[u][i] = buf[ab + i * 16 * a.wrow + oa + u * sa];
+#pragma unroll
+                for (int b = 0; b < NPB; ++b) o.B[u][b] = buf[bb[b] + ob + u * sb];
+            }
+        };
+        auto mma = [&](const Ops &o) {
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int i = 0; i < TKB; ++i)
+#pragma unroll
+                    for (int b = 0; b < NPB; ++b) {
+                        acc[i][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.A[u][i], o.B[u][b],
+                                                                        acc[i][b], 0, 0, 0);
+                        // one LDS read between consecutive MFMAs
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    }
+        };
+        Ops o[2];
+        load(0, o[0]);
+        int j = 0;
+        for (; j + 2 <= tg; j += 2) {
+            load(j + 1, o[1]);
+            mma(o[0]);
+            load(j + 2, o[0]);
+            mma(o[1]);
+        }
+        if (j < tg) mma(o[0]);
+    }
+
+    // wave groups 1..KG-1 hand their partial tiles to group 0 through LDS
+    if constexpr (KG > 1) {
+        __syncthreads();
+        floatx4 *red = reinterpret_cast<floatx4 *>(smem);
+        constexpr int per_wave = 64 * TKB * NPB;
+        if (g > 0) {
+            floatx4 *dst = red + ((g - 1) * a.wpx + wp) * per_wave;
+#pragma unroll
+            for (int i = 0; i < TKB; ++i)
+#pragma unroll
+                for (int b = 0; b < NPB; ++b) dst[(i * NPB + b) * 64 + lane] = acc[i][b];
+        }
+        __syncthreads();
+        if (g > 0) return;
+#pragma unroll
+        for (int h = 1; h < KG; ++h) {
+            const floatx4 *src = red + ((h - 1) * a.wpx + wp) * per_wave;
+#pragma unroll
+            for (int i = 0; i < TKB; ++i)
+#pragma unroll
+                for (int b = 0; b < NPB; ++b) acc[i][b] += src[(i * NPB + b) * 64 + lane];
+        }
+    }
+    // 16x16 block: lane holds rows 4*lg + v (channels), column li (pixel)
+    float *yn = (a.ksw > 1 ? a.part + (size_t)z * a.N * a.K * PQ : a.y) + (size_t)n * a.K * PQ;
+#pragma unroll
+    for (int i = 0; i < TKB; ++i)
+#pragma unroll
+        for (int b = 0; b < NPB; ++b) {
+            if (!pv[b]) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int k = kt * a.tk + i * 16 + 4 * lg + v;
+                if (k < a.K) yn[(size_t)k * PQ + oq[b]] = acc[i][b][v];
+            }
+        }
+}
+
 // ---- instance registry --------------------------------------------------------
 // conv_valu slots: ((log2 KPT * 5 + log2 PPT) * 5 + log2 UF) * 2 + LDS
 // conv_mfma slots: ((log2 TKB * 7 + log2 NPB) * 3 + D - 1) * 2 + LDS
+// conv_mfma2 slots: ((log2 TKB * 6 + log2 NPB) * 3 + log2 U) * 3 + log2 KG
 constexpr int kValuSlots = kConvValuSlots;
 constexpr int kMfmaSlots = kConvMfmaSlots;
 
@@ -751,6 +1052,7 @@ constexpr int kMfmaSlots = kConvMfmaSlots;
 
 extern const void *g_conv_valu[kConvValuSlots];
 extern const void *g_conv_mfma[kConvMfmaSlots];
+extern const void *g_conv_mfma2[kConvMfma2Slots];
 
 #ifndef DS_SLICE
 #define DS_SLICE 0
@@ -776,6 +1078,19 @@ void reg_mfma() {
         g_conv_mfma[I] = reinterpret_cast<const void *>(&conv_mfma<TKB, NPB, D, lds>);
 }
 
+template <int I>
+void reg_mfma2() {
+    constexpr int ikg = I % 3, iu = (I / 3) % 3, inpb = (I / 9) % 6, itkb = I / 54;
+    constexpr int TKB = 1 << itkb, NPB = 1 << inpb, U = 1 << iu, KG = 1 << ikg;
+    if constexpr (conv2_regs_ok(TKB, NPB, KG) && I % DS_NSLICES == DS_SLICE)
+        g_conv_mfma2[I] = reinterpret_cast<const void *>(&conv_mfma2<TKB, NPB, U, KG>);
+}
+
+template <size_t... I>
+void reg_all_mfma2(std::index_sequence<I...>) {
+    (reg_mfma2<int(I)>(), ...);
+}
+
 template <size_t... I>
 void reg_all(std::index_sequence<I...>) {
     (reg_valu<int(I)>(), ...);
@@ -789,6 +1104,7 @@ struct Registrar {
     Registrar() {
         reg_all(std::make_index_sequence<kValuSlots>{});
         reg_all_mfma(std::make_index_sequence<kMfmaSlots>{});
+        reg_all_mfma2(std::make_index_sequence<kConvMfma2Slots>{});
     }
 };
 const Registrar registrar;

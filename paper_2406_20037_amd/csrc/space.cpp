@@ -21,6 +21,7 @@ const int32_t kSplit[] = {1, 2, 4, 8};
 const int32_t kMmTile[] = {16, 32, 64, 128, 256};
 const int32_t kMmBk[] = {4, 8, 16, 32, 64};
 const int32_t kOnOff[] = {0, 1};
+const int32_t kConvMfma[] = {0, 1, 2};
 const int32_t kVec[] = {1, 4};
 
 const char *kConvNames[] = {"tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma", "vec"};
@@ -69,6 +70,27 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
     Geometry g;
     const int npx = th * tw;
     const int outs = tk * npx;
+    if (mfma == 2) {
+        // channel-quad MFMA family: LDS staging only; its unroll depth is
+        // taken like the other MFMA family's (3 from 16 unrolled steps, 2
+        // from 4), over its 16x16 blocks
+        const int body2 = std::max(1, tk / 16) * std::max(1, npx / (16 * std::min(4, std::max(1, npx / 16))));
+        const int ue = unroll == 0 ? 1 : std::min(16, pow2_floor(std::max(1, unroll / body2)));
+        const int depth = ue >= 16 ? 3 : (ue >= 4 ? 2 : 1);
+        Conv2Args a;
+        const Conv2Shape c = conv2_setup(sh, tk, th, tw, tc, depth, ks, vec, a);
+        g.threads = c.threads;
+        g.grid = c.grid;
+        g.lds_bytes = int(std::min<int64_t>(c.lds, INT32_MAX));
+        g.acc = 4 * c.tkb * c.npb;
+        g.unroll_eff = depth;
+        g.t0 = c.tkb;
+        g.t1 = c.npb;
+        g.red = c.red;
+        g.chunks = a.chunks;
+        g.valid = c.valid && lds == 1;
+        return g;
+    }
     bool ok;
     int body, wrow;
     if (!mfma) {
@@ -304,7 +326,7 @@ int build_space(int op, const int64_t *sh, int shape_len, Space &sp) {
         for (int i = 0; i < 9; ++i) sp.shape[i] = sh[i];
         sp.values = {clipped(kPow2to64, K), clipped(kPow2to64, P), clipped(kPow2to64, Q),
                      clipped(kPow2to64, C), all_of(kUnroll), all_of(kOnOff),
-                     clipped(kSplit, C), all_of(kOnOff),       all_of(kVec)};
+                     clipped(kSplit, C), all_of(kConvMfma),    all_of(kVec)};
         sp.names.assign(kConvNames, kConvNames + 9);
     } else if (op == DS_OP_MATMUL_RM) {
         if (shape_len != 3) {

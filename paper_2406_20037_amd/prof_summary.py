@@ -39,7 +39,7 @@ def source_hash(kernel: str) -> str | None:
 
 
 # Position of the unroll-factor template argument of each kernel family.
-UNROLL_ARG = {"mm_mfma": 3, "mm_valu": 3, "conv_mfma": 2, "conv_valu": 2}
+UNROLL_ARG = {"mm_mfma": 3, "mm_valu": 3, "conv_mfma": 2, "conv_valu": 2, "conv_mfma2": 2}
 
 
 def traffic_key(kernel: str, sched: str, shape=None) -> str:
@@ -65,7 +65,8 @@ def traffic_key(kernel: str, sched: str, shape=None) -> str:
 
 def short(name: str) -> str:
     return (name.replace("ds::(anonymous namespace)::", "").replace("void ", "")
-            .replace("(ds::MatmulArgs)", "").replace("(ds::ConvArgs)", ""))
+            .replace("(ds::MatmulArgs)", "").replace("(ds::ConvArgs)", "")
+            .replace("(ds::Conv2Args)", ""))
 
 
 def top_kernels(db, top):

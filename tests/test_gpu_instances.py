@@ -32,7 +32,7 @@ pytestmark = pytest.mark.gpu
 LDS_LIMIT = 163840
 CANARY = 12345.0
 TAIL = 64
-FAMILY = {1: "conv_valu", 2: "conv_mfma", 3: "mm_valu", 4: "mm_mfma"}
+FAMILY = {1: "conv_valu", 2: "conv_mfma", 3: "mm_valu", 4: "mm_mfma", 5: "conv_mfma2"}
 
 
 @pytest.fixture(scope="module")

@@ -55,8 +55,8 @@ def test_value_lists_named_shapes():
     assert s0.values[0] == [1, 2, 4, 8, 16, 32, 64]
     assert s0.values[1] == [1, 2, 4, 8, 16, 32] == s0.values[2]
     assert s0.values[3] == [1, 2, 4, 8, 16, 32, 64]
-    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1], [1, 4]]
-    assert s0.size() == 7 * 6 * 6 * 7 * 4 * 2 * 4 * 2 * 2
+    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1, 2], [1, 4]]
+    assert s0.size() == 7 * 6 * 6 * 7 * 4 * 2 * 4 * 3 * 2
     s2 = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
     assert s2.values[1] == [1, 2, 4, 8, 16, 32, 64]       # P = 112
     assert s2.values[3] == [1, 2] and s2.values[6] == [1, 2]
@@ -169,6 +169,48 @@ def test_conv_mfma_small_tile_geometry():
     c = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
     g = c.geometry(idx_of(c, tk=16, th=4, tw=8, tc=16, unroll=0, lds=1, ks=1, mfma=1, vec=4))
     assert g["valid"] and g["threads"] == 128 and g["t1"] == 1
+
+
+def test_conv_quad_geometry_hand_computed():
+    """mfma = 2 (channel-quad steps), worked by hand from the layout rules."""
+    s = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
+    # 64 pixels over four waves, one 16x16 block each; unroll 64 over one
+    # block -> u = 16 -> depth 3 -> 4 quads per step.  All 64 channels in one
+    # chunk: 16 quads; ks = 2 -> two wave groups (16 % (2 * 4) == 0, 512
+    # threads), no split across workgroups.  Halo 6 rows of 24 (aligned:
+    # 15 + 3 + 3 -> 24), channel stride 144 (= 16 mod 32); weight rows of
+    # 16 * 9 = 144 -> 145 (odd) * 4 = 580 floats.  One buffer of
+    # 16 * 580 + 64 * 144 = 18496 floats.  Copy units per thread:
+    # 2320 / 512 and 2304 / 512 -> 5.
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=64, lds=1, ks=2, mfma=2, vec=4))
+    assert g == dict(valid=True, grid=4 * 14 * 4, threads=512, lds_bytes=4 * 18496, acc=4,
+                     unroll_eff=3, t0=1, t1=1, red=576, chunks=1)
+    # the same tile with unroll 0 (one quad per step) and ks = 4: four wave
+    # groups of four waves, 64 * 4 * 4 = 1024 threads
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
+    assert g["valid"] and g["threads"] == 1024 and g["grid"] == 224
+    # 8-channel chunks hold 2 quads: unroll 64 (4 quads per step) does not fit
+    # them; with one quad per step and ks = 4 the groups fall back to two
+    # (2 % 4 != 0), the remaining factor 2 splits across workgroups
+    assert not s.valid(idx_of(s, tk=16, th=4, tw=16, tc=8, unroll=64, lds=1, ks=1, mfma=2, vec=4))
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=8, unroll=0, lds=1, ks=4, mfma=2, vec=4))
+    assert g["valid"] and g["threads"] == 512 and g["grid"] == 2 * 224 and g["chunks"] == 8
+    # chunks of whole quads: tc = 2 on 64 channels is not; LDS staging only
+    assert not s.valid(idx_of(s, tk=16, th=4, tw=16, tc=2, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    assert not s.valid(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=0, lds=0, ks=1, mfma=2, vec=1))
+    # register budget of four wave groups: at most 4 blocks per wave (4 x 2
+    # blocks do not fit, 2 x 2 do)
+    assert not s.valid(idx_of(s, tk=64, th=8, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
+    assert s.valid(idx_of(s, tk=32, th=8, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
+    # The 3-channel stem: tc = 1 stands for the single chunk of all three
+    # channels (one quad, channel 3 zero); 256 pixels -> four blocks per wave;
+    # halo 7 * 2 + 7 = 21 rows of 31 * 2 + 7 + 3 -> 72 (aligned), channel
+    # stride 1512 -> 1520 (= 16 mod 32); weight rows 49 (odd) * 4 = 196.
+    st = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
+    g = st.geometry(idx_of(st, tk=16, th=8, tw=32, tc=1, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    assert g == dict(valid=True, grid=4 * 14 * 4, threads=256, lds_bytes=4 * (16 * 196 + 4 * 1520),
+                     acc=16, unroll_eff=1, t0=1, t1=4, red=196, chunks=1)
+    assert not st.valid(idx_of(st, tk=16, th=8, tw=32, tc=2, unroll=0, lds=1, ks=1, mfma=2, vec=4))
 
 
 def test_matmul_geometry_hand_computed():
