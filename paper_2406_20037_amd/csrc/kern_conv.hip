@@ -834,8 +834,12 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
     // never read); halo rows of the channel padding read any valid float
     // (never read); -1: nothing to copy (past the buffer, or outside the
     // image: left zero).
+    // (held only when the workgroup walks more than one chunk: a single
+    // chunk's units are computed as they are issued, so the first copies leave
+    // sooner)
+    const bool reuse = a.regs && ci1 - ci0 > 1;
     int sw[kConv2RegCopies], sh[kConv2RegCopies];
-    if (a.regs) {
+    if (reuse) {
         q4::Cursor cur;
         cur.start(a, tid);
         const int gw = a.vw ? 4 : 1, gh = a.vh ? 4 : 1;
@@ -875,8 +879,9 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
         }
     };
     // Units computed as they are issued: a chunk with channel slots past C
-    // (its buffer zeroed first), or every chunk when a thread's units do not
-    // fit its registers (4-byte copies of misaligned operands).
+    // (its buffer zeroed first), a workgroup's only chunk, or every chunk when
+    // a thread's units do not fit its registers (4-byte copies of misaligned
+    // operands).
     auto issue_units = [&](int ci, int b, bool zero) {
         float *wt = smem + b * a.buf;
         float *xs = wt + a.bufw;
@@ -919,7 +924,7 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
     }
     auto issue = [&](int ci, int b) {
         if (creal_of(ci) < tc4) issue_units(ci, b, true);
-        else if (a.regs) issue_full(ci, b);
+        else if (reuse) issue_full(ci, b);
         else issue_units(ci, b, false);
     };
     issue(ci0, 0);
