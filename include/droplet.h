@@ -162,7 +162,7 @@ int sched_has_kernel(const ds_space *space, const ds_sched *s);
 /* Kernel families (the sketches whose annotations the spaces enumerate). */
 enum {
     DS_KERNEL_CONV_VALU = 1,  /* conv_valu<KPT, PPT, UF, LDS> */
-    DS_KERNEL_CONV_MFMA = 2,  /* conv_mfma<TKB, NPB, UF, LDS> */
+    DS_KERNEL_CONV_MFMA = 2,  /* conv_mfma<TKB, NPB, D, LDS> (conv mfma = 1) */
     DS_KERNEL_MM_VALU = 3,    /* mm_valu<RM, RN, BK, UF, DB> */
     DS_KERNEL_MM_MFMA = 4,    /* mm_mfma<WM, WN, BK, UF, DB, KG> */
     DS_KERNEL_CONV_MFMA2 = 5  /* conv_mfma2<TKB, NPB, U, KG> (conv mfma = 2) */

@@ -40,7 +40,7 @@ STATUS_NAMES = {0: "DS_OK", -1: "DS_EINVAL", -2: "DS_EUNSUPPORTED", -3: "DS_EINV
 
 DS_OP_CONV2D_NCHW = 1
 DS_OP_MATMUL_RM = 2
-DS_KERNEL_CONV_VALU, DS_KERNEL_CONV_MFMA, DS_KERNEL_MM_VALU, DS_KERNEL_MM_MFMA = 1, 2, 3, 4
+DS_KERNEL_CONV_VALU, DS_KERNEL_CONV_MFMA, DS_KERNEL_MM_VALU, DS_KERNEL_MM_MFMA, DS_KERNEL_CONV_MFMA2 = 1, 2, 3, 4, 5
 DS_MAX_KNOBS = 12
 DS_MAX_REPEATS = 64
 DS_NOALLOC_MAX_FLOATS = 8388608   # kernel_run_noalloc: split partials capacity
