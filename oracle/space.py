@@ -83,6 +83,17 @@ def _clip(values, extent):
     return kept if kept else [min(values)]
 
 
+def _cover(values, extent):
+    """The clipped list plus the smallest value >= extent when that value
+    is larger than every kept one (a tile spanning a whole output row or
+    column)."""
+    kept = _clip(values, extent)
+    above = [v for v in values if v >= extent]
+    if above and min(above) > kept[-1]:
+        kept = kept + [min(above)]
+    return kept
+
+
 def _cdiv(a, b):
     return -(-a // b)
 
@@ -202,7 +213,7 @@ class Space(Lattice):
             N, C, H, W, K, R, S, st, pd = shape
             P, Q = conv_out(shape)
             values = [
-                _clip(POW2_64, K), _clip(POW2_64, P), _clip(POW2_64, Q), _clip(POW2_64, C),
+                _clip(POW2_64, K), _cover(POW2_64, P), _cover(POW2_64, Q), _clip(POW2_64, C),
                 list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1, 2], list(VEC),
             ]
             names = CONV_AXES
@@ -228,6 +239,10 @@ def conv_geometry(shape, v):
     N, C, H, W, K, R, S, st, pd = shape
     P, Q = conv_out(shape)
     tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
+    if th > P or tw > Q:
+        # tiles past the output's height or width exist only as mfma = 2 bands
+        return dict(valid=False, grid=0, threads=0, lds_bytes=0, acc=0, unroll_eff=1, t0=0,
+                    t1=0, red=0, chunks=0)
     npx = th * tw
     outs = tk * npx
     if v["mfma"] == 0:
@@ -315,20 +330,33 @@ def conv_quad_geometry(shape, v):
     largest of 4, 2, 1 not above ks whose U-blocks of quads divide the chunk's
     quads and that keeps 1024 threads), the rest across workgroups.
 
+    A tile at least as wide as the output (tw >= Q) is a band: th * tw
+    consecutive pixels of the output flattened over (image, row, column).
+    Image n's output row p reads padded rows n * hp + p * st + r with
+    hp = (P - 1) * st + R, so a band's halo is one range of padded rows, each
+    one output row wide; the grid is ks / KG * (K / tk) * (N P Q / (th tw))
+    rounded up.  A band spans at most D = min(N P, 1 + ceil((npx - 1) / Q))
+    output rows (at least one) with at most X = min(N - 1, ceil((D - 1) / P)) image
+    boundaries among them: consecutive rows are st padded rows apart, R across
+    a boundary, so hs = (D - 1) st + X max(0, R - st) + R.  Other tiles are
+    th x tw rectangles of one image with th <= P.
+
     LDS per buffer: tk weight rows of wrow floats (the smallest 4 * odd >=
-    4 * quads * R * S) and 4 * quads halo channels of cs floats (the smallest
-    >= hs * ws that is 16 mod 32); two buffers when a workgroup walks more than
-    one chunk; the wave groups' partial tiles reuse it.  Validity adds: at
-    least one 16x16 block, chunks of whole channel quads (tc >= 4, or tc = 1
-    standing for all channels of an image with fewer than four), LDS staging,
-    the register budget of the compiled instances (at most 32, 16, 4 blocks
-    per wave and 20, 12, 8 channel plus pixel blocks for KG = 1, 2, 4), and
-    at most 12 copy units per thread per kind
-    for a full chunk (4-byte units, or 16-byte ones where rows allow: vec).
+    4 * quads * R * S with 16-byte weight copies, else the smallest 2 * odd)
+    and 4 * quads halo channels of cs floats (the smallest >= hs * ws that is
+    16 mod 32); two buffers when a workgroup walks more than one chunk; the
+    wave groups' partial tiles reuse it.  Validity adds: at least one 16x16
+    block, chunks of whole channel quads (tc >= 4, or tc = 1 standing for all
+    channels of an image with fewer than four), LDS staging, the register
+    budget of the compiled instances (at most 32, 16, 4 blocks per wave and
+    20, 12, 8 channel plus pixel blocks for KG = 1, 2, 4), at most 12 copy
+    units per thread per kind for a full chunk (4-byte units, or 16-byte ones
+    where rows allow: vec), and copy offsets below 2^29 floats.
     """
     N, C, H, W, K, R, S, st, pd = shape
     P, Q = conv_out(shape)
     tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
+    band = tw >= Q
     npx = th * tw
     waves = min(4, max(1, npx // 16))
     tkb, npb = max(1, tk // 16), max(1, npx // (16 * waves))
@@ -339,6 +367,7 @@ def conv_quad_geometry(shape, v):
     chan = C if C < 4 else tc                  # real channels of a full chunk
     quads = _cdiv(chan, 4)
     ok = tk >= 16 and npx >= 16 and (tc >= 4 or (C < 4 and tc == 1))
+    ok = ok and (band or th <= P)
     kg = min(v["ks"], 4)
     while kg > 1 and (quads % (kg * quads_per_step) or 64 * waves * kg > THREADS_LIMIT):
         kg //= 2
@@ -348,15 +377,25 @@ def conv_quad_geometry(shape, v):
     chunks = _cdiv(C, chan)
     cps = _cdiv(chunks, ksw)
     ok = ok and ksw <= chunks
-    hs = (th - 1) * st + R
-    halo16 = v["vec"] == 4 and W % 4 == 0 and tw * st >= 16
-    ws = _cdiv((tw - 1) * st + S + 3, 4) * 4 if halo16 else (tw - 1) * st + S
+    if band:
+        d = max(1, min(N * P, 1 + _cdiv(npx - 1, Q)))
+        x = min(N - 1, _cdiv(d - 1, P))
+        hs = (d - 1) * st + max(0, x) * max(0, R - st) + R
+        cols = Q
+    else:
+        hs = (th - 1) * st + R
+        cols = tw
+    halo16 = v["vec"] == 4 and W % 4 == 0 and cols * st >= 16
+    ws = _cdiv((cols - 1) * st + S + 3, 4) * 4 if halo16 else (cols - 1) * st + S
     cs = hs * ws
     while cs % 32 != 16:
         cs += 1
-    half_row = quads * R * S                   # weight row floats / 4
-    wrow = 4 * (half_row if half_row % 2 else half_row + 1)
     w16 = v["vec"] == 4 and (C * R * S) % 4 == 0 and (chan * R * S) % 4 == 0
+    unit = 4 if w16 else 2
+    odd = _cdiv(4 * quads * R * S, unit)
+    if odd % 2 == 0:
+        odd += 1
+    wrow = unit * odd
     ok = ok and (v["vec"] == 1 or w16 or halo16)
     threads = 64 * waves * kg
     units_w = tk * wrow // 4 if w16 else tk * wrow
@@ -366,7 +405,14 @@ def conv_quad_geometry(shape, v):
     nbuf = 2 if cps > 1 else 1
     buf = tk * wrow + 4 * quads * cs
     lds = max(4 * nbuf * buf, 16 * (kg - 1) * waves * 64 * blocks)
-    grid = N * ksw * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)
+    if band:
+        grid = ksw * _cdiv(K, tk) * _cdiv(N * P * Q, npx)
+        images = min(N, 1 + _cdiv(npx - 1, P * Q))
+        ok = ok and (images * C + 4 * quads) * H * W < 2 ** 29
+    else:
+        grid = N * ksw * _cdiv(K, tk) * _cdiv(P, th) * _cdiv(Q, tw)
+        ok = ok and 4 * quads * H * W < 2 ** 29
+    ok = ok and tk * C * R * S < 2 ** 29
     valid = (ok and v["lds"] == 1 and lds <= LDS_LIMIT and threads <= THREADS_LIMIT
              and grid <= GRID_LIMIT)
     return dict(valid=valid, grid=grid, threads=threads, lds_bytes=lds, acc=4 * blocks,

@@ -137,10 +137,17 @@ struct Conv2Args {
     int N, C, H, W, K, R, S, st, pd, P, Q;
     int tk, th, tw, tc;   // tc: real channels of a full chunk (C when C < 4)
     int tiles_k, tiles_p, tiles_q, ksw;   // ksw: reduction splits across workgroups
+                          //    (band tiles: tiles_p = 1, tiles_q = bands, no image axis)
+    int band;             // band tiles (tw >= Q): a tile is th * tw consecutive pixels of
+                          //    the flattened (image, row, column) output space
+    int hp;               // band tiles: padded rows per image, (P - 1) * st + R; image n's
+                          //    output row p reads padded rows n * hp + p * st + r
+    int F;                // band tiles: N * P * Q
     int chunks, cps;      // reduction chunks, chunks per split
     int t4;               // channel quads per chunk (channel slots / 4)
     int hs, ws, cs;       // halo rows, halo row stride, halo channel stride (floats)
-    int wrow;             // weight row stride (floats, 4 * odd)
+    int wrow;             // weight row stride (floats; 4 * odd for 16-byte weight copies,
+                          //    else 2 * odd)
     int npx, ltw, wpx, lwpx;   // tile pixels, log2(tw), pixel waves and log2
     int bufw, buf;        // floats of the weight part of a buffer, of a whole buffer
     int nbuf;             // LDS buffers (2 when a workgroup walks more than one chunk)
@@ -154,6 +161,7 @@ struct Conv2Args {
     int w_dk, w_dc;       // blockDim in (weight row, unit) mixed radix
     int h_dc, h_dr;       // blockDim in (halo channel, unit) mixed radix
     FastDiv f_wru, f_hcu, f_hru, f_rs, f_s, f_tk, f_tq, f_tp, f_ksw;
+    FastDiv f_q, f_p, f_hp;   // band tiles: Q, P, hp
 };
 
 // Launch shape of a conv_mfma2 point.
@@ -190,15 +198,30 @@ inline void conv2_units(Conv2Args &a, int threads) {
     a.f_wru = make_fastdiv(a.wr_u); a.f_hcu = make_fastdiv(a.hc_u); a.f_hru = make_fastdiv(a.hr_u);
 }
 
+// Halo rows of a band of npx consecutive output pixels (flattened over
+// image, row, column): it spans at most D output rows, and consecutive rows
+// are st padded rows apart inside an image and R across an image boundary
+// (image n's rows start at n * hp, hp = (P - 1) * st + R), so the padded
+// rows it reads number at most (D - 1) * st + X * max(0, R - st) + R with X
+// the image boundaries among its D rows.
+inline int64_t conv2_band_rows(int64_t N, int64_t P, int64_t Q, int64_t R, int64_t st, int64_t npx) {
+    const int64_t d = std::max<int64_t>(1, std::min(N * P, 1 + (npx - 1 + Q - 1) / Q));
+    const int64_t x = std::min(N - 1, (d - 1 + P - 1) / P);
+    return (d - 1) * st + std::max<int64_t>(0, x) * std::max<int64_t>(0, R - st) + R;
+}
+
 // Set-up of conv_mfma2 for shape sh and knob values (depth D = 1..3 from the
 // unroll knob; the k-steps unrolled per loop step are U = 2^(D-1) quads).
 // The in-workgroup reduction split KG is the largest of 4, 2, 1 not above ks
 // that divides the quads of a chunk into whole U-blocks and fits 1024
-// threads; the rest of ks splits across workgroups.  Fills a (buffers aside)
-// and returns the shape with its validity: a tile of at least one 16x16
-// block, chunks of whole channel quads (tc >= 4, or for fewer than four
-// image channels tc = 1 standing for all of them), the register budget of
-// the compiled instances (no spill), the copy units a thread holds, LDS.
+// threads; the rest of ks splits across workgroups.  A tile at least as wide
+// as the output (tw >= Q) is a band: th * tw consecutive pixels of the
+// flattened output, across row and image boundaries, whose halo is a range
+// of padded rows.  Fills a (buffers aside) and returns the shape with its
+// validity: a tile of at least one 16x16 block, chunks of whole channel quads
+// (tc >= 4, or for fewer than four image channels tc = 1 standing for all of
+// them), the register budget of the compiled instances (no spill), the copy
+// units a thread holds, LDS, and copy offsets within 31 bits.
 inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc, int depth, int ks,
                               int vec, Conv2Args &a) {
     Conv2Shape g;
@@ -210,6 +233,8 @@ inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc,
     a.tk = tk; a.th = th; a.tw = tw;
     const int RS = a.R * a.S;
     bool ok = tk >= 16 && th * tw >= 16 && (tc >= 4 || (a.C < 4 && tc == 1));
+    a.band = tw >= a.Q;
+    ok = ok && (a.band || th <= a.P);
     a.tc = a.C < 4 ? a.C : tc;
     const int tc4 = (a.tc + 3) / 4 * 4;
     a.t4 = tc4 / 4;
@@ -231,16 +256,27 @@ inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc,
     a.chunks = int((a.C + a.tc - 1) / a.tc);
     a.cps = (a.chunks + a.ksw - 1) / a.ksw;
     ok = ok && a.ksw <= a.chunks;
-    a.hs = (th - 1) * a.st + a.R;
-    const bool halo16 = vec == 4 && a.W % 4 == 0 && int64_t(tw) * a.st >= 16;
-    a.ws = halo16 ? int(((int64_t(tw - 1) * a.st + a.S + 3 + 3) / 4) * 4) : (tw - 1) * a.st + a.S;
-    int64_t cs = int64_t(a.hs) * a.ws;
+    const int64_t span_w = a.band ? a.Q : tw;         // output columns a halo row covers
+    int64_t hs = int64_t(th - 1) * a.st + a.R;
+    if (a.band) {
+        hs = conv2_band_rows(a.N, a.P, a.Q, a.R, a.st, a.npx);
+        a.hp = (a.P - 1) * a.st + a.R;
+    }
+    a.hs = int(std::min<int64_t>(hs, INT32_MAX));
+    const bool halo16 = vec == 4 && a.W % 4 == 0 && span_w * a.st >= 16;
+    a.ws = int(halo16 ? ((span_w - 1) * a.st + a.S + 3 + 3) / 4 * 4 : (span_w - 1) * a.st + a.S);
+    int64_t cs = hs * a.ws;
     cs += ((16 - cs % 32) + 32) % 32;                 // cs = 16 mod 32: the four lane groups'
     a.cs = int(std::min<int64_t>(cs, INT32_MAX));     // channels fall on disjoint banks
-    int64_t r4 = (int64_t(tc4) * RS + 3) / 4;
-    if (r4 % 2 == 0) ++r4;                            // rows 4*odd floats apart: the 16 rows of
-    a.wrow = int(std::min<int64_t>(4 * r4, INT32_MAX));   // a block fall on disjoint banks
     a.vw = vec == 4 && (int64_t(a.C) * RS) % 4 == 0 && (int64_t(a.tc) * RS) % 4 == 0;
+    // Weight rows: the 16 rows of a block are read together, one float each,
+    // by lanes of the same channel, 32 lanes at a time.  4 * odd floats apart
+    // (16-byte copies need rows of whole 16-byte groups) puts them on 8 banks
+    // of each 4-bank group; 2 * odd puts them on 16 distinct banks.
+    const int64_t unit = a.vw ? 4 : 2;
+    int64_t odd = (int64_t(tc4) * RS + unit - 1) / unit;
+    if (odd % 2 == 0) ++odd;
+    a.wrow = int(std::min<int64_t>(unit * odd, INT32_MAX));
     a.hal = halo16;
     a.vh = halo16;
     ok = ok && (vec == 1 || a.vw || a.vh);
@@ -254,13 +290,30 @@ inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc,
     // slots past C, C < 4, compute theirs as they go)
     ok = ok && (a.C < 4 || a.regs);
     a.tiles_k = int((a.K + tk - 1) / tk);
-    a.tiles_p = int((a.P + th - 1) / th);
-    a.tiles_q = int((a.Q + tw - 1) / tw);
+    int64_t grid;
+    if (a.band) {
+        const int64_t F = int64_t(a.N) * a.P * a.Q;
+        a.F = int(std::min<int64_t>(F, INT32_MAX));
+        a.tiles_p = 1;
+        a.tiles_q = int((F + a.npx - 1) / a.npx);
+        grid = int64_t(a.ksw) * a.tiles_k * a.tiles_q;
+        // copy offsets from the band's first image: at most `imgs` images
+        const int64_t imgs = std::min<int64_t>(a.N, 1 + (a.npx - 1 + int64_t(a.P) * a.Q - 1) /
+                                                          (int64_t(a.P) * a.Q));
+        ok = ok && (imgs * a.C + tc4) * int64_t(a.H) * a.W < (int64_t(1) << 29);
+    } else {
+        a.tiles_p = int((a.P + th - 1) / th);
+        a.tiles_q = int((a.Q + tw - 1) / tw);
+        grid = int64_t(a.N) * a.ksw * a.tiles_k * a.tiles_p * a.tiles_q;
+        ok = ok && int64_t(tc4) * a.H * a.W < (int64_t(1) << 29);
+    }
+    ok = ok && int64_t(tk) * a.C * RS < (int64_t(1) << 29);
     a.f_rs = make_fastdiv(RS); a.f_s = make_fastdiv(a.S);
-    a.f_tk = make_fastdiv(a.tiles_k); a.f_tq = make_fastdiv(a.tiles_q);
+    a.f_tk = make_fastdiv(a.tiles_k); a.f_tq = make_fastdiv(std::max(1, a.tiles_q));
     a.f_tp = make_fastdiv(a.tiles_p); a.f_ksw = make_fastdiv(a.ksw);
+    a.f_q = make_fastdiv(a.Q); a.f_p = make_fastdiv(a.P); a.f_hp = make_fastdiv(std::max(1, a.hp));
     g.lds = std::max<int64_t>(4 * int64_t(a.nbuf) * buf, int64_t(16) * (kg - 1) * a.wpx * 64 * body);
-    g.grid = int64_t(a.N) * a.ksw * a.tiles_k * a.tiles_p * a.tiles_q;
+    g.grid = grid;
     g.red = tc4 * RS;
     g.valid = ok && g.lds <= kLdsLimit && g.threads <= kThreadsLimit && g.grid <= kGridLimit;
     return g;

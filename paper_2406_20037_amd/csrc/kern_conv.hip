@@ -820,12 +820,40 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
     const int PQ = a.P * a.Q;
     const int slot = wu * 64;
     const int tc4 = 4 * a.t4;
+    // A band tile starts at pixel qt * npx of the flattened output: image n0,
+    // padded row g0 of that image; its halo is the `rows` padded rows from
+    // there (image boundaries included), each one whole output row wide.
+    int n0 = n, g0 = 0, rows = a.hs;
+    if (a.band) {
+        const int f0 = qt * a.npx, fl = min(f0 + a.npx, a.F) - 1;
+        const int r0 = fdv(f0, a.f_q), rl = fdv(fl, a.f_q);
+        n0 = fdv(r0, a.f_p);
+        const int nl = fdv(rl, a.f_p);
+        g0 = (r0 - n0 * a.P) * a.st;
+        rows = (nl - n0) * a.hp + (rl - nl * a.P) * a.st + a.R - g0;
+    }
     const int hy0 = pt * a.th * a.st - a.pd;
-    const int hx0 = a.hal ? (qt * a.tw * a.st - a.pd) & ~3 : qt * a.tw * a.st - a.pd;
+    const int col0 = (a.band ? 0 : qt * a.tw * a.st) - a.pd;
+    const int hx0 = a.hal ? col0 & ~3 : col0;
     const int kvalid = a.K - kt * a.tk;
     const float *wk = a.w + (size_t)kt * a.tk * a.C * RS;
-    const float *xn = a.x + (size_t)n * a.C * a.H * a.W;
+    const float *xn = a.x + (size_t)n0 * a.C * a.H * a.W;
     auto creal_of = [&](int ci) { return min(a.tc, a.C - ci * a.tc); };
+    // Float offset of halo position (channel hc, row hy, column hx) from the
+    // chunk's first channel of image n0, or -1 outside the image (left zero).
+    auto halo_src = [&](int hc, int hy, int hx) {
+        int gy, img = 0;
+        if (a.band) {
+            const int gr = g0 + hy;
+            img = fdv(gr, a.f_hp);
+            gy = gr - img * a.hp - a.pd;
+        } else {
+            gy = hy0 + hy;
+        }
+        const int gx = hx0 + hx;
+        const bool in = hy < rows && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+        return in ? ((img * a.C + hc) * a.H + gy) * a.W + gx : -1;
+    };
 
     // Copy sources of a full chunk (byte offsets from its weight / image
     // base, the same for every full chunk): thread t's u-th unit of a kind is
@@ -852,9 +880,8 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
                 sw[u] = cur.kl < a.tk ? 4 * (kl * a.C * RS + col) : -1;
                 const int hy = fdv(cur.hu, a.f_hru);
                 const int hx = gh * (cur.hu - hy * a.hr_u);
-                const int gy = hy0 + hy, gx = hx0 + hx;
-                const bool in = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
-                sh[u] = cur.hc >= tc4 ? -1 : hy >= a.hs ? 0 : in ? 4 * ((cur.hc * a.H + gy) * a.W + gx) : -1;
+                const int o = halo_src(cur.hc, hy, hx);
+                sh[u] = cur.hc >= tc4 ? -1 : hy >= a.hs ? 0 : o >= 0 ? 4 * o : -1;
                 cur.next(a);
             }
         }
@@ -905,21 +932,26 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
             }
             const int hy = fdv(cur.hu, a.f_hru);
             const int hx = gh * (cur.hu - hy * a.hr_u);
-            const int gy = hy0 + hy, gx = hx0 + hx;
-            if (cur.hc < creal && hy < a.hs && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W) {
-                const unsigned o = unsigned(4 * ((cur.hc * a.H + gy) * a.W + gx));
-                if (a.vh) q4::copy<16>(xb, o, xs + 4 * d);
-                else q4::copy<4>(xb, o, xs + d);
+            const int o = halo_src(cur.hc, hy, hx);
+            if (cur.hc < creal && hy < a.hs && o >= 0) {
+                if (a.vh) q4::copy<16>(xb, unsigned(4 * o), xs + 4 * d);
+                else q4::copy<4>(xb, unsigned(4 * o), xs + d);
             }
         }
     };
 
-    // Halo positions outside the image are never copied: zero every buffer
-    // once when the tile's halo reaches past the image.
-    const bool border = hy0 < 0 || hy0 + a.hs > a.H || hx0 < 0 || hx0 + a.ws > a.W;
+    // Halo positions outside the image are never copied: zero the halo part
+    // of every buffer once when the tile's halo reaches past the image (a
+    // band's does wherever there is zero padding).
+    const bool border = a.band ? a.pd > 0
+                               : hy0 < 0 || hy0 + a.hs > a.H || hx0 < 0 || hx0 + a.ws > a.W;
     if (border) {
-        for (int e = tid; e < a.nbuf * a.buf / 4; e += nthr)
-            reinterpret_cast<floatx4 *>(smem)[e] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const int per = (a.buf - a.bufw) / 4;
+        for (int e = tid; e < a.nbuf * per; e += nthr) {
+            const int b = e >= per ? 1 : 0;
+            reinterpret_cast<floatx4 *>(smem + b * a.buf + a.bufw)[e - b * per] =
+                floatx4{0.f, 0.f, 0.f, 0.f};
+        }
         __syncthreads();
     }
     auto issue = [&](int ci, int b) {
@@ -932,15 +964,26 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
     // lane bases (floats) inside a buffer
     int bb[NPB], oq[NPB];
     bool pv[NPB];
-    const int shift = a.hal ? (qt * a.tw * a.st - a.pd) & 3 : 0;
+    const int shift = a.hal ? col0 & 3 : 0;
 #pragma unroll
     for (int b = 0; b < NPB; ++b) {
         const int pix = (wp * NPB + b) * 16 + li;
-        const int py = pix >> a.ltw, px = pix & (a.tw - 1);
-        const int p = pt * a.th + py, q = qt * a.tw + px;
-        pv[b] = pix < a.npx && p < a.P && q < a.Q;
-        bb[b] = a.bufw + lg * a.cs + py * a.st * a.ws + px * a.st + shift;
-        oq[b] = p * a.Q + q;
+        if (a.band) {
+            // pixels past the output read the last one's operands (discarded)
+            const int f = qt * a.npx + pix;
+            const int fc = min(f, a.F - 1);
+            const int r = fdv(fc, a.f_q), q = fc - r * a.Q;
+            const int img = fdv(r, a.f_p), p = r - img * a.P;
+            pv[b] = f < a.F;
+            bb[b] = a.bufw + lg * a.cs + ((img - n0) * a.hp + p * a.st - g0) * a.ws + q * a.st + shift;
+            oq[b] = img * a.K * PQ + p * a.Q + q;
+        } else {
+            const int py = pix >> a.ltw, px = pix & (a.tw - 1);
+            const int p = pt * a.th + py, q = qt * a.tw + px;
+            pv[b] = pix < a.npx && p < a.P && q < a.Q;
+            bb[b] = a.bufw + lg * a.cs + py * a.st * a.ws + px * a.st + shift;
+            oq[b] = p * a.Q + q;
+        }
     }
     const int ab = li * a.wrow + lg * RS;
     const int sa = 4 * KG * RS, sb = 4 * KG * a.cs;   // quad strides of one group

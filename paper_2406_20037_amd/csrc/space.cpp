@@ -39,6 +39,19 @@ std::vector<int32_t> clipped(const int32_t (&list)[L], int64_t extent) {
     return out;
 }
 
+// The clipped list plus the smallest value that covers `extent`, if the list
+// has one above it: a tile may span a whole output row or column.
+template <size_t L>
+std::vector<int32_t> covering(const int32_t (&list)[L], int64_t extent) {
+    std::vector<int32_t> out = clipped(list, extent);
+    for (int32_t v : list)
+        if (v >= extent) {
+            if (v > out.back()) out.push_back(v);
+            break;
+        }
+    return out;
+}
+
 // Largest value of the clipped list.
 template <size_t L>
 int64_t clipped_max(const int32_t (&list)[L], int64_t extent) {
@@ -91,6 +104,8 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         g.valid = c.valid && lds == 1;
         return g;
     }
+    // tiles past the output's height or width exist only as band tiles
+    if (th > P || tw > Q) return g;
     bool ok;
     int body, wrow;
     if (!mfma) {
@@ -324,7 +339,7 @@ int build_space(int op, const int64_t *sh, int shape_len, Space &sp) {
             return DS_EUNSUPPORTED;
         }
         for (int i = 0; i < 9; ++i) sp.shape[i] = sh[i];
-        sp.values = {clipped(kPow2to64, K), clipped(kPow2to64, P), clipped(kPow2to64, Q),
+        sp.values = {clipped(kPow2to64, K), covering(kPow2to64, P), covering(kPow2to64, Q),
                      clipped(kPow2to64, C), all_of(kUnroll), all_of(kOnOff),
                      clipped(kSplit, C), all_of(kConvMfma),    all_of(kVec)};
         sp.names.assign(kConvNames, kConvNames + 9);

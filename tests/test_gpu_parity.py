@@ -217,6 +217,53 @@ def test_parity_misaligned_operands(torch_dev, lib, shift_x, shift_w):
             assert np.array_equal(out, ref), f"{sh} shift x {shift_x} w {shift_w} {o.knobs(p)}"
 
 
+BAND_CASES = [
+    ("band_14_cross", (2, 16, 14, 14, 32, 3, 3, 1, 1)),
+    ("band_7_multi", (3, 8, 7, 7, 16, 3, 3, 1, 1)),
+    ("band_1x1_s2", (1, 16, 56, 56, 32, 1, 1, 2, 0)),
+    ("band_3x3_s2", (2, 16, 28, 28, 16, 3, 3, 2, 1)),
+    ("band_c3_7x7_s2", (2, 3, 20, 20, 16, 7, 7, 2, 3)),
+    ("band_odd", (2, 12, 13, 13, 20, 3, 3, 1, 1)),
+    ("band_pad0", (2, 20, 9, 9, 24, 3, 3, 1, 0)),
+    ("band_5x5", (2, 4, 30, 30, 17, 5, 5, 1, 2)),
+    ("band_wide", (1, 8, 5, 40, 16, 3, 3, 1, 1)),
+]
+
+
+@pytest.mark.parametrize("name,sh", BAND_CASES, ids=[c[0] for c in BAND_CASES])
+def test_parity_band_tiles(torch_dev, lib, name, sh):
+    """mfma = 2 band tiles (tw >= Q: runs of consecutive output pixels across
+    rows and images): small-integer inputs, so every schedule must match the
+    oracle exactly; every output written and nothing past the end.  Half the
+    points also run on operands 4 bytes past a 16-byte boundary."""
+    torch = torch_dev
+    x, w = synthdata.conv_inputs(sh, "int")
+    ref = ok.conv2d_f64(x, w, sh).ravel()
+    r = Runner(torch_dev, lib, 1, sh, x, w)
+    o = osp.Space(1, sh)
+    Q = osp.conv_out(sh)[1]
+    pts = [p for p in o.valid_points() if o.knobs(p)["mfma"] == 2 and o.knobs(p)["tw"] >= Q]
+    assert pts
+    rng = np.random.default_rng(zlib.crc32(name.encode()) % 1000)
+    if len(pts) > 120:
+        pts = [pts[i] for i in sorted(rng.choice(len(pts), 120, replace=False))]
+    xs = torch.zeros(x.size + 1, dtype=torch.float32, device="cuda:0")
+    xs[1:] = torch.from_numpy(np.ascontiguousarray(x).ravel()).to("cuda:0")
+    ws = torch.zeros(w.size + 1, dtype=torch.float32, device="cuda:0")
+    ws[1:] = torch.from_numpy(np.ascontiguousarray(w).ravel()).to("cuda:0")
+    y = torch.empty(ref.size, dtype=torch.float32, device="cuda:0")
+    space = lib.Space(1, sh)
+    for i, p in enumerate(pts):
+        print(name, o.knobs(p), flush=True)
+        assert np.array_equal(r.run(p), ref), f"{name} {o.knobs(p)}"
+        if i % 2:
+            y.fill_(float("nan"))
+            lib.kernel_run(1, space.sched(p), xs[1:], ws[1:], y)
+            torch.cuda.synchronize()
+            out = y.cpu().numpy().astype(np.float64)
+            assert np.array_equal(out, ref), f"{name} misaligned {o.knobs(p)}"
+
+
 def test_empty_batch_and_rows(torch_dev, lib):
     torch = torch_dev
     s = lib.Space(1, (0, 4, 8, 8, 4, 3, 3, 1, 1))
@@ -247,6 +294,8 @@ MODEL_SCHEDULES = [
     dict(tk=16, th=4, tw=16, tc=8, unroll=16, lds=1, ks=2, mfma=1, vec=4),
     dict(tk=8, th=4, tw=8, tc=8, unroll=16, lds=1, ks=1, mfma=0, vec=1),
     dict(tk=16, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1, vec=1),
+    dict(tk=64, th=8, tw=32, tc=16, unroll=512, lds=1, ks=1, mfma=2, vec=4),
+    dict(tk=64, th=4, tw=64, tc=8, unroll=16, lds=1, ks=2, mfma=2, vec=4),
 ]
 
 

@@ -53,12 +53,17 @@ def test_key_mixed_radix():
 def test_value_lists_named_shapes():
     s0 = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
     assert s0.values[0] == [1, 2, 4, 8, 16, 32, 64]
-    assert s0.values[1] == [1, 2, 4, 8, 16, 32] == s0.values[2]
+    # P = Q = 56: tile heights and widths up to 32, and 64 that covers a row
+    assert s0.values[1] == [1, 2, 4, 8, 16, 32, 64] == s0.values[2]
     assert s0.values[3] == [1, 2, 4, 8, 16, 32, 64]
     assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1, 2], [1, 4]]
-    assert s0.size() == 7 * 6 * 6 * 7 * 4 * 2 * 4 * 3 * 2
+    assert s0.size() == 7 * 7 * 7 * 7 * 4 * 2 * 4 * 3 * 2
+    s14 = sp.Space(sp.OP_CONV, (16, 512, 14, 14, 512, 3, 3, 1, 1))
+    assert s14.values[1] == [1, 2, 4, 8, 16] == s14.values[2]
+    s32 = sp.Space(sp.OP_CONV, (1, 8, 32, 32, 16, 3, 3, 1, 1))
+    assert s32.values[1] == [1, 2, 4, 8, 16, 32] == s32.values[2]   # 32 covers 32
     s2 = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
-    assert s2.values[1] == [1, 2, 4, 8, 16, 32, 64]       # P = 112
+    assert s2.values[1] == [1, 2, 4, 8, 16, 32, 64]       # P = 112: nothing covers it
     assert s2.values[3] == [1, 2] and s2.values[6] == [1, 2]
     m = sp.Space(sp.OP_MATMUL, (1024, 1024, 1024))
     assert m.values == [[16, 32, 64, 128, 256]] * 2 + [[4, 8, 16, 32, 64], [0, 16, 64, 512],
@@ -205,12 +210,50 @@ def test_conv_quad_geometry_hand_computed():
     # The 3-channel stem: tc = 1 stands for the single chunk of all three
     # channels (one quad, channel 3 zero); 256 pixels -> four blocks per wave;
     # halo 7 * 2 + 7 = 21 rows of 31 * 2 + 7 + 3 -> 72 (aligned), channel
-    # stride 1512 -> 1520 (= 16 mod 32); weight rows 49 (odd) * 4 = 196.
+    # stride 1512 -> 1520 (= 16 mod 32); 3 * 49 weights per filter are not
+    # whole 16-byte groups, so weight rows take 4-byte copies and are
+    # 2 * odd floats: 4 * 49 = 196 -> 98 (even) -> 99 * 2 = 198.
     st = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
     g = st.geometry(idx_of(st, tk=16, th=8, tw=32, tc=1, unroll=0, lds=1, ks=1, mfma=2, vec=4))
-    assert g == dict(valid=True, grid=4 * 14 * 4, threads=256, lds_bytes=4 * (16 * 196 + 4 * 1520),
+    assert g == dict(valid=True, grid=4 * 14 * 4, threads=256, lds_bytes=4 * (16 * 198 + 4 * 1520),
                      acc=16, unroll_eff=1, t0=1, t1=4, red=196, chunks=1)
     assert not st.valid(idx_of(st, tk=16, th=8, tw=32, tc=2, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+
+
+def test_conv_band_geometry_hand_computed():
+    """mfma = 2 band tiles (tw >= Q), worked by hand."""
+    # VGG-16 L11 (16 images of 512 x 14 x 14): tw = 16 covers a row, so a
+    # tile is a band of 8 * 16 = 128 consecutive output pixels.  Four waves
+    # of two 16-pixel blocks, four channel blocks; 8-channel chunks: 2 quads,
+    # 64 chunks, two buffers.  A band spans at most 1 + ceil(127 / 14) = 11
+    # output rows with at most one image boundary among them: 10 + 1 * 2 + 3
+    # = 15 padded rows of 13 + 3 = 16 floats (W % 4 != 0: 4-byte halo
+    # copies), channel stride 240 (= 16 mod 32).  Weight rows: 8 * 9 = 72
+    # floats -> 18 (even) -> 19 * 4 = 76 (16-byte copies).  Buffer 64 * 76 +
+    # 8 * 240 = 6784 floats; copy units per thread: 1216 / 256 -> 5 and
+    # 1920 / 256 -> 8.  Grid: 8 channel tiles x ceil(3136 / 128) = 25 bands.
+    v = sp.Space(sp.OP_CONV, (16, 512, 14, 14, 512, 3, 3, 1, 1))
+    g = v.geometry(idx_of(v, tk=64, th=8, tw=16, tc=8, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    assert g == dict(valid=True, grid=200, threads=256, lds_bytes=4 * 2 * 6784, acc=32,
+                     unroll_eff=1, t0=4, t1=2, red=72, chunks=64)
+    # tiles past the height are bands only; the other families have no such
+    # tiles at all
+    assert not v.valid(idx_of(v, tk=64, th=16, tw=8, tc=8, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    g = v.geometry(idx_of(v, tk=64, th=8, tw=16, tc=8, unroll=0, lds=1, ks=1, mfma=1, vec=4))
+    assert g == dict(valid=False, grid=0, threads=0, lds_bytes=0, acc=0, unroll_eff=1, t0=0,
+                     t1=0, red=0, chunks=0)
+    # Stride 2, 1 x 1 (ResNet-50 downsampling, one image of 256 x 56 x 56 to
+    # 28 x 28): tw = 32 covers 28; bands of 4 * 32 = 128 pixels span at most
+    # 1 + ceil(127 / 28) = 6 rows of one image: 5 * 2 + 1 = 11 padded rows of
+    # 27 * 2 + 1 + 3 -> 60 floats (aligned, 16-byte copies), channel stride
+    # 660 -> 688.  Weight rows 16 -> 4 (even) -> 5 * 4 = 20.  Copy units per
+    # thread: 160 / 256 -> 1 and 4 * 688 / 256 -> 11.  Buffer 32 * 20 +
+    # 16 * 688 = 11648 floats, two of them; grid 16 x ceil(784 / 128) = 7.
+    r = sp.Space(sp.OP_CONV, (1, 256, 56, 56, 512, 1, 1, 2, 0))
+    g = r.geometry(idx_of(r, tk=32, th=4, tw=32, tc=16, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    assert g == dict(valid=True, grid=112, threads=256, lds_bytes=4 * 2 * 11648, acc=16,
+                     unroll_eff=1, t0=2, t1=2, red=16, chunks=16)
+
 
 
 def test_matmul_geometry_hand_computed():
