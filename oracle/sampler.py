@@ -1,26 +1,31 @@
 """Reference exploration sampler (test infrastructure only).
 
 The exploration phase of the combined approach (Section 2.3, step 1) measures
-the first N schedules that Ansor produces.  Ansor draws initial annotations from
-per-rule probability distributions (Section 2.1, "The Initialization of
-Annotations"); that figure is missing from the paper, so the reading here is
-the uniform distribution over each axis, drawn without replacement over valid
-points:
+the first N schedules that Ansor produces.  Ansor builds that initial
+population by annotating its sketches (Section 2.1, "Sketch annotation" and
+"The Initialization of Annotations"); the figure with the per-rule
+distributions is missing from the paper, so the reading here is: a sketch is
+chosen uniformly, then an annotation uniformly among the sketch's valid ones,
+without replacement.  The kernel family (the ``mfma`` knob of the conv and
+matmul spaces) stands for the sketch; a generic lattice is one sketch.
 
-1. Each draw picks an index on every axis in axis order.  The index on an axis
-   with n values is ``z mod n`` for the next SplitMix64 output z, redrawn while
+1. The valid points of each family are listed in key order.
+2. Each draw takes index ``below(F)`` among the F families that still have an
+   undrawn valid point (in family order), then index ``below(M)`` among that
+   family's M undrawn points, and removes the point.  ``below(n)`` is
+   ``z mod n`` for the next SplitMix64 output z, redrawn while
    ``z >= floor(2**64 / n) * n`` so that every index is equally likely.
-2. A drawn point that is invalid or was already drawn is rejected.
-3. Sampling stops after ``n_explore`` distinct valid points or after
-   ``100 * n_explore`` drawn points, whichever comes first.
+3. Sampling stops after ``n_explore`` points or when every valid point has
+   been drawn.
 
 SplitMix64 is re-implemented here from its published definition (Steele, Lea
 and Flood, OOPSLA 2014) on Python integers; it shares no code with the library
 or with ``synthdata``.
 
 Pins (tests/test_oracle_sampler.py): the published SplitMix64 sequence for
-seed 1234567, determinism, no duplicates, ``min(n, |valid|)`` points, and a
-chi-square uniformity test on a small lattice.
+seed 1234567, determinism, no duplicates, ``min(n, |valid|)`` points, and
+chi-square tests that the family of a first draw is uniform over the families
+with a valid point and that the point is uniform within its family.
 """
 from __future__ import annotations
 
@@ -46,17 +51,41 @@ class SplitMix64:
                 return z % n
 
 
+def sketch_axis(space):
+    """Axis of the kernel-family knob of a conv or matmul space; None for a
+    generic lattice."""
+    return space.names.index("mfma") if hasattr(space, "op") else None
+
+
+class Stream:
+    """The draw sequence of one space and seed, taken incrementally."""
+
+    def __init__(self, space, seed):
+        axis = sketch_axis(space)
+        families = {}
+        for p in space.valid_points():               # key order
+            families.setdefault(0 if axis is None else p[axis], []).append(p)
+        self.pools = [families[f] for f in sorted(families)]
+        self.rng = SplitMix64(seed)
+
+    def next(self):
+        """The next point, or None once every valid point has been drawn."""
+        live = [pool for pool in self.pools if pool]
+        if not live:
+            return None
+        pool = live[self.rng.below(len(live))]
+        return pool.pop(self.rng.below(len(pool)))
+
+
 def sample(space, seed, n_explore):
     """Distinct valid points in draw order."""
-    rng = SplitMix64(seed)
-    seen = set()
     out = []
-    draws = 0
-    while len(out) < n_explore and draws < 100 * n_explore:
-        draws += 1
-        idx = tuple(rng.below(n) for n in space.sizes)
-        if idx in seen or not space.valid(idx):
-            continue
-        seen.add(idx)
-        out.append(idx)
+    if n_explore <= 0:
+        return out
+    stream = Stream(space, seed)
+    while len(out) < n_explore:
+        p = stream.next()
+        if p is None:
+            break
+        out.append(p)
     return out

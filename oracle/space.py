@@ -198,7 +198,7 @@ class Lattice:
         return None
 
     def valid_points(self):
-        return [self.from_key(k) for k in range(self.size()) if self.valid(self.from_key(k))]
+        return [p for p in map(self.from_key, range(self.size())) if self.valid(p)]
 
 
 class Space(Lattice):

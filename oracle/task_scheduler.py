@@ -32,33 +32,26 @@ from __future__ import annotations
 import math
 
 from .droplet import Meas, droplet
-from .sampler import SplitMix64
+from .sampler import Stream
 
 
 class _Stream:
     """The exploration sampler's draw sequence, consumed incrementally."""
 
     def __init__(self, space, seed):
-        self.space = space
-        self.rng = SplitMix64(seed)
-        self.seen = set()
-        self.draws = 0
+        self.stream = Stream(space, seed)
         self.taken = 0
         self.ended = False
 
     def take(self, n):
         out = []
-        target = self.taken + n
-        while self.taken < target and self.draws < 100 * target:
-            self.draws += 1
-            idx = tuple(self.rng.below(m) for m in self.space.sizes)
-            if idx in self.seen or not self.space.valid(idx):
-                continue
-            self.seen.add(idx)
-            self.taken += 1
-            out.append(idx)
-        if self.taken < target:
-            self.ended = True
+        while len(out) < n:
+            p = self.stream.next()
+            if p is None:
+                self.ended = True
+                break
+            out.append(p)
+        self.taken += len(out)
         return out
 
 

@@ -95,23 +95,53 @@ void trace_push(ds_trace *tr, int stage, const Meas &m, uint64_t key) {
 
 using MeasureFn = std::function<Meas(const int32_t *idx, double best_so_far)>;
 
-// The draw sequence of the exploration sampler.
+// The draw sequence of the exploration sampler (Section 2.1, sketch
+// annotation; Section 2.3, step 1).  The kernel family -- the mfma knob of
+// the conv and matmul spaces -- stands for the sketch: each draw first picks
+// a family uniformly among those that still have an undrawn valid point,
+// then one of that family's undrawn valid points uniformly (in key order,
+// removed once drawn).  A generic lattice is a single family.  Sampling stops
+// at n_explore points or when every valid point has been drawn.
+int sketch_axis(const Space &sp) {
+    if (sp.op == DS_OP_CONV2D_NCHW) return 7;
+    if (sp.op == DS_OP_MATMUL_RM) return 5;
+    return -1;
+}
+
+struct ExploreSampler {
+    const Space &sp;
+    SplitMix64 rng;
+    std::vector<std::vector<uint64_t>> pool;   // undrawn valid keys per family, key order
+    std::vector<int> live;
+    ExploreSampler(const Space &s, uint64_t seed) : sp(s), rng(seed) {
+        const int sa = sketch_axis(sp);
+        pool.resize(sa < 0 ? 1 : sp.values[sa].size());
+        std::vector<int32_t> idx(sp.nknobs);
+        for (uint64_t k = 0; k < sp.size; ++k) {
+            sp.from_key(k, idx.data());
+            if (sp.geometry(idx.data()).valid) pool[sa < 0 ? 0 : idx[sa]].push_back(k);
+        }
+    }
+    // The next point, or false once every valid point has been drawn.
+    bool next(int32_t *idx) {
+        live.clear();
+        for (size_t f = 0; f < pool.size(); ++f)
+            if (!pool[f].empty()) live.push_back(int(f));
+        if (live.empty()) return false;
+        std::vector<uint64_t> &p = pool[live[rng.below(uint32_t(live.size()))]];
+        const uint32_t j = rng.below(uint32_t(p.size()));
+        sp.from_key(p[j], idx);
+        p.erase(p.begin() + j);
+        return true;
+    }
+};
+
 std::vector<std::vector<int32_t>> draw_points(const Space &sp, uint64_t seed, int n_explore) {
     std::vector<std::vector<int32_t>> out;
     if (n_explore <= 0) return out;
-    SplitMix64 rng(seed);
-    std::unordered_set<uint64_t> seen;
-    int64_t draws = 0;
-    const int64_t max_draws = 100 * int64_t(n_explore);
+    ExploreSampler smp(sp, seed);
     std::vector<int32_t> idx(sp.nknobs);
-    while (int(out.size()) < n_explore && draws < max_draws) {
-        ++draws;
-        for (int a = 0; a < sp.nknobs; ++a) idx[a] = int32_t(rng.below(uint32_t(sp.values[a].size())));
-        const uint64_t k = sp.key(idx.data());
-        if (seen.count(k) || !sp.geometry(idx.data()).valid) continue;
-        seen.insert(k);
-        out.push_back(idx);
-    }
+    while (int(out.size()) < n_explore && smp.next(idx.data())) out.push_back(idx);
     return out;
 }
 
@@ -918,9 +948,7 @@ int ds_tune_tasks(const ds_task *tasks, int n_tasks, int total_trials, const ds_
         const Space *sp = nullptr;
         float *owned = nullptr;
         MeasureFn measure;
-        std::unique_ptr<SplitMix64> rng;
-        std::unordered_set<uint64_t> seen;
-        int64_t draws = 0;
+        std::unique_ptr<ExploreSampler> smp;
         int taken = 0;
         bool ended = false;
         Cache cache;
@@ -939,7 +967,7 @@ int ds_tune_tasks(const ds_task *tasks, int n_tasks, int total_trials, const ds_
         if (rc != DS_OK) break;
         T.measure = make_measure(*T.sp, &cfg, &tasks[t].io,
                                  T.owned ? T.owned : tasks[t].io.ref, tasks[t].fn, tasks[t].ctx);
-        T.rng.reset(new SplitMix64(tasks[t].seed));
+        T.smp.reset(new ExploreSampler(*T.sp, tasks[t].seed));
     }
     auto release = [&]() {
         for (auto &T : st) free_device(T.owned);
@@ -959,13 +987,8 @@ int ds_tune_tasks(const ds_task *tasks, int n_tasks, int total_trials, const ds_
         const int target = T.taken + n;
         std::vector<int32_t> idx(sp.nknobs);
         int got = 0;
-        while (T.taken < target && T.draws < 100 * int64_t(target)) {
-            ++T.draws;
-            for (int a = 0; a < sp.nknobs; ++a)
-                idx[a] = int32_t(T.rng->below(uint32_t(sp.values[a].size())));
+        while (T.taken < target && T.smp->next(idx.data())) {
             const uint64_t k = sp.key(idx.data());
-            if (T.seen.count(k) || !sp.geometry(idx.data()).valid) continue;
-            T.seen.insert(k);
             T.taken++;
             got++;
             Meas m = T.measure(idx.data(), T.best_so_far);

@@ -59,3 +59,33 @@ def test_first_draw_uniform_over_lattice():
     firsts = [lat.key(sm.sample(lat, seed, 1)[0]) for seed in range(6000)]
     counts = np.bincount(firsts, minlength=15)
     assert stats.chisquare(counts).pvalue > 0.01
+
+
+class _FamilySpace(sp.Lattice):
+    """A small space with a kernel-family axis: family 0 has 12 valid
+    points, family 1 has 3, family 2 none."""
+    op = 0
+
+    def __init__(self):
+        super().__init__([[0, 1, 2], [0, 1, 2, 3], [0, 1, 2]], names=["a", "b", "mfma"],
+                         predicate=lambda p: p[2] == 0 or (p[2] == 1 and p[1] == 0))
+
+
+def test_first_draw_uniform_over_families_then_within():
+    s = _FamilySpace()
+    firsts = [sm.sample(s, seed, 1)[0] for seed in range(6000)]
+    fam = np.bincount([p[2] for p in firsts], minlength=3)
+    assert fam[2] == 0 and stats.chisquare(fam[:2]).pvalue > 0.01
+    for f, n in ((0, 12), (1, 3)):
+        within = [s.key(p) for p in firsts if p[2] == f]
+        counts = np.unique(within, return_counts=True)[1]
+        assert len(counts) == n and stats.chisquare(counts).pvalue > 0.01
+
+
+def test_families_drawn_until_exhausted():
+    s = _FamilySpace()
+    got = sm.sample(s, 5, 100)
+    assert sorted(got) == sorted(s.valid_points()) and len(got) == 15
+    # the small family is used up after a few draws; the rest come from family 0
+    assert sum(1 for p in got[:6] if p[2] == 1) >= 1
+
