@@ -101,7 +101,7 @@ def bench_check(db, bench_json):
     at = sorted(d for d, g in durs if threads is None or g == threads)
     print(f"\n### Dominant kernel of the profiled bench.py run\n")
     print(f"bench.py: `{kname}` on task {rf['task']}, average launch {rf['avg_launch_us']:.3f} us "
-          f"(events over the timed graph launches), {rf['achieved']} {rf['unit']} "
+          f"(events around its launches in the timed passes), {rf['achieved']} {rf['unit']} "
           f"= {rf['frac']:.3f} of {rf['peak']}.\n")
     if not at:
         print("No traced dispatch of that kernel at that launch shape.")
