@@ -58,10 +58,24 @@ def test_two_streams_split_concurrently(env):
     close(torch, b)
 
 
-def test_capture_after_the_workspace_exists(env):
+SPLIT_CASES = [
+    ((1, 64, 40, 40, 64, 3, 3, 1, 1),
+     dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1, vec=4)),
+    # channel-quad family, band tiles, four splits across workgroups
+    ((2, 32, 14, 14, 64, 3, 3, 1, 1),
+     dict(tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=4, mfma=2, vec=4)),
+    # rectangular tiles, two wave groups and two splits across workgroups
+    ((1, 64, 40, 40, 64, 3, 3, 1, 1),
+     dict(tk=16, th=4, tw=16, tc=8, unroll=0, lds=1, ks=4, mfma=2, vec=4)),
+]
+
+
+@pytest.mark.parametrize("sh,knobs", SPLIT_CASES, ids=["mfma1", "mfma2_band", "mfma2_kg2"])
+def test_capture_after_the_workspace_exists(env, sh, knobs):
+    """Graph replays of a captured split schedule (main kernel and reduce
+    launch) give the eager result bit for bit, on both MFMA conv families."""
     torch, L = env
-    c = conv_case(torch, L, (1, 64, 40, 40, 64, 3, 3, 1, 1),
-                  dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1, vec=4))
+    c = conv_case(torch, L, sh, knobs)
     st = torch.cuda.Stream()
     # first call outside capture creates this stream's workspace
     L.kernel_run(L.DS_OP_CONV2D_NCHW, c["s"], c["x"], c["w"], c["y"], st)
