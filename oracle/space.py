@@ -15,13 +15,16 @@ two lattices below are readings:
 conv2d (op 1), shape (N, C, H, W, K, R, S, stride, pad), axes in order
     tk, th, tw, tc in {1, 2, 4, ..., 64}: output-tile extent along K, P, Q and
         the input-channel chunk of one reduction step; kept if <= K, P, Q, C
-        (the smallest value is always kept);
+        (the smallest value is always kept), and th, tw also keep the smallest
+        value >= P, Q (only band tiles, mfma 3, may reach past the output);
     unroll in {0, 16, 64, 512}: maximum unrolled steps of the reduction loop;
     lds in {0, 1}: stage input and weight tiles in LDS;
     ks in {1, 2, 4, 8}: reduction split over C across workgroups (kept if <= C);
-    mfma in {0, 1, 2}: contract on VALU FMA (0) or fp32 MFMA (implicit GEMM):
-        1 steps through 16-step groups of the (c, r, s) reduction, 2 through
-        (tap, channel quad) steps (a second MFMA sketch, LDS staging only);
+    mfma in {0, 1, 2, 3}: contract on VALU FMA (0) or fp32 MFMA (implicit
+        GEMM): 1 steps through 16-step groups of the (c, r, s) reduction, 2
+        through (tap, channel quad) steps over rectangular tiles (a second MFMA
+        sketch, LDS staging only), 3 the same over band tiles (the pixel loops
+        fused over image, row and column before tiling);
     vec in {1, 4}: floats per lane of the global -> LDS copies (4 or 16 bytes).
 
 matmul (op 2), shape (M, N, K), axes in order
@@ -214,7 +217,7 @@ class Space(Lattice):
             P, Q = conv_out(shape)
             values = [
                 _clip(POW2_64, K), _cover(POW2_64, P), _cover(POW2_64, Q), _clip(POW2_64, C),
-                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1, 2], list(VEC),
+                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1, 2, 3], list(VEC),
             ]
             names = CONV_AXES
         else:
@@ -234,13 +237,13 @@ class Space(Lattice):
 
 
 def conv_geometry(shape, v):
-    if v["mfma"] == 2:
+    if v["mfma"] >= 2:
         return conv_quad_geometry(shape, v)
     N, C, H, W, K, R, S, st, pd = shape
     P, Q = conv_out(shape)
     tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
     if th > P or tw > Q:
-        # tiles past the output's height or width exist only as mfma = 2 bands
+        # tiles past the output's height or width exist only as mfma = 3 bands
         return dict(valid=False, grid=0, threads=0, lds_bytes=0, acc=0, unroll_eff=1, t0=0,
                     t1=0, red=0, chunks=0)
     npx = th * tw
@@ -321,7 +324,7 @@ def conv_geometry(shape, v):
 
 
 def conv_quad_geometry(shape, v):
-    """mfma = 2: implicit GEMM whose k-steps each take one channel quad (four
+    """mfma = 2 and 3: implicit GEMM whose k-steps each take one channel quad (four
     consecutive input channels) at one tap (r, s), over LDS-staged weights and
     input halo.  Waves split the tile's pixels as for mfma = 1 (16x16 blocks,
     up to four pixel waves); the unroll knob gives the depth D (3 from 16
@@ -330,16 +333,17 @@ def conv_quad_geometry(shape, v):
     largest of 4, 2, 1 not above ks whose U-blocks of quads divide the chunk's
     quads and that keeps 1024 threads), the rest across workgroups.
 
-    A tile at least as wide as the output (tw >= Q) is a band: th * tw
-    consecutive pixels of the output flattened over (image, row, column).
+    mfma = 2 tiles are th x tw rectangles of one image (th <= P, tw <= Q).
+    mfma = 3 tiles are bands: th * tw consecutive pixels of the output
+    flattened over (image, row, column), the pixel loops fused before tiling
+    (a sketch of its own).
     Image n's output row p reads padded rows n * hp + p * st + r with
     hp = (P - 1) * st + R, so a band's halo is one range of padded rows, each
     one output row wide; the grid is ks / KG * (K / tk) * (N P Q / (th tw))
     rounded up.  A band spans at most D = min(N P, 1 + ceil((npx - 1) / Q))
     output rows (at least one) with at most X = min(N - 1, ceil((D - 1) / P)) image
     boundaries among them: consecutive rows are st padded rows apart, R across
-    a boundary, so hs = (D - 1) st + X max(0, R - st) + R.  Other tiles are
-    th x tw rectangles of one image with th <= P.
+    a boundary, so hs = (D - 1) st + X max(0, R - st) + R.
 
     LDS per buffer: tk weight rows of wrow floats (the smallest 4 * odd >=
     4 * quads * R * S with 16-byte weight copies, else the smallest 2 * odd)
@@ -356,7 +360,7 @@ def conv_quad_geometry(shape, v):
     N, C, H, W, K, R, S, st, pd = shape
     P, Q = conv_out(shape)
     tk, th, tw, tc = v["tk"], v["th"], v["tw"], v["tc"]
-    band = tw >= Q
+    band = v["mfma"] == 3
     npx = th * tw
     waves = min(4, max(1, npx // 16))
     tkb, npb = max(1, tk // 16), max(1, npx // (16 * waves))
@@ -367,7 +371,7 @@ def conv_quad_geometry(shape, v):
     chan = C if C < 4 else tc                  # real channels of a full chunk
     quads = _cdiv(chan, 4)
     ok = tk >= 16 and npx >= 16 and (tc >= 4 or (C < 4 and tc == 1))
-    ok = ok and (band or th <= P)
+    ok = ok and (band or (th <= P and tw <= Q))
     kg = min(v["ks"], 4)
     while kg > 1 and (quads % (kg * quads_per_step) or 64 * waves * kg > THREADS_LIMIT):
         kg //= 2

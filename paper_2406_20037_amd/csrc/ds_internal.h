@@ -214,16 +214,17 @@ inline int64_t conv2_band_rows(int64_t N, int64_t P, int64_t Q, int64_t R, int64
 // unroll knob; the k-steps unrolled per loop step are U = 2^(D-1) quads).
 // The in-workgroup reduction split KG is the largest of 4, 2, 1 not above ks
 // that divides the quads of a chunk into whole U-blocks and fits 1024
-// threads; the rest of ks splits across workgroups.  A tile at least as wide
-// as the output (tw >= Q) is a band: th * tw consecutive pixels of the
-// flattened output, across row and image boundaries, whose halo is a range
-// of padded rows.  Fills a (buffers aside) and returns the shape with its
+// threads; the rest of ks splits across workgroups.  Rectangular tiles
+// (band false) are th x tw pixels of one image, within its P x Q; band tiles
+// are th * tw consecutive pixels of the output flattened over (image, row,
+// column), across row and image boundaries, whose halo is a range of padded
+// rows.  Fills a (buffers aside) and returns the shape with its
 // validity: a tile of at least one 16x16 block, chunks of whole channel quads
 // (tc >= 4, or for fewer than four image channels tc = 1 standing for all of
 // them), the register budget of the compiled instances (no spill), the copy
 // units a thread holds, LDS, and copy offsets within 31 bits.
 inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc, int depth, int ks,
-                              int vec, Conv2Args &a) {
+                              int vec, bool band, Conv2Args &a) {
     Conv2Shape g;
     a = Conv2Args();
     a.N = int(sh[0]); a.C = int(sh[1]); a.H = int(sh[2]); a.W = int(sh[3]); a.K = int(sh[4]);
@@ -233,8 +234,8 @@ inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc,
     a.tk = tk; a.th = th; a.tw = tw;
     const int RS = a.R * a.S;
     bool ok = tk >= 16 && th * tw >= 16 && (tc >= 4 || (a.C < 4 && tc == 1));
-    a.band = tw >= a.Q;
-    ok = ok && (a.band || th <= a.P);
+    a.band = band;
+    ok = ok && (band || (th <= a.P && tw <= a.Q));
     a.tc = a.C < 4 ? a.C : tc;
     const int tc4 = (a.tc + 3) / 4 * 4;
     a.t4 = tc4 / 4;

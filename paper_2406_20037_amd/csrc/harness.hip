@@ -486,11 +486,12 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
     plan.threads = g.threads;
     plan.grid = g.grid;
     plan.lds = g.lds_bytes;
-    if (s->op == DS_OP_CONV2D_NCHW && sp.value(s->idx, 7) == 2) {
+    if (s->op == DS_OP_CONV2D_NCHW && sp.value(s->idx, 7) >= 2) {
         Conv2Args &a = plan.conv2;
         const Conv2Shape c = conv2_setup(sp.shape, sp.value(s->idx, 0), sp.value(s->idx, 1),
                                          sp.value(s->idx, 2), sp.value(s->idx, 3), g.unroll_eff,
-                                         sp.value(s->idx, 6), sp.value(s->idx, 8), a);
+                                         sp.value(s->idx, 6), sp.value(s->idx, 8),
+                                         sp.value(s->idx, 7) == 3, a);
         a.x = x;
         a.w = w;
         a.y = y;

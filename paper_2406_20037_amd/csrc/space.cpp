@@ -21,7 +21,7 @@ const int32_t kSplit[] = {1, 2, 4, 8};
 const int32_t kMmTile[] = {16, 32, 64, 128, 256};
 const int32_t kMmBk[] = {4, 8, 16, 32, 64};
 const int32_t kOnOff[] = {0, 1};
-const int32_t kConvMfma[] = {0, 1, 2};
+const int32_t kConvMfma[] = {0, 1, 2, 3};
 const int32_t kVec[] = {1, 4};
 
 const char *kConvNames[] = {"tk", "th", "tw", "tc", "unroll", "lds", "ks", "mfma", "vec"};
@@ -83,15 +83,16 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
     Geometry g;
     const int npx = th * tw;
     const int outs = tk * npx;
-    if (mfma == 2) {
-        // channel-quad MFMA family: LDS staging only; its unroll depth is
-        // taken like the other MFMA family's (3 from 16 unrolled steps, 2
-        // from 4), over its 16x16 blocks
+    if (mfma >= 2) {
+        // channel-quad MFMA family (mfma 2: rectangular tiles, mfma 3: band
+        // tiles): LDS staging only; its unroll depth is taken like the other
+        // MFMA family's (3 from 16 unrolled steps, 2 from 4), over its 16x16
+        // blocks
         const int body2 = std::max(1, tk / 16) * std::max(1, npx / (16 * std::min(4, std::max(1, npx / 16))));
         const int ue = unroll == 0 ? 1 : std::min(16, pow2_floor(std::max(1, unroll / body2)));
         const int depth = ue >= 16 ? 3 : (ue >= 4 ? 2 : 1);
         Conv2Args a;
-        const Conv2Shape c = conv2_setup(sh, tk, th, tw, tc, depth, ks, vec, a);
+        const Conv2Shape c = conv2_setup(sh, tk, th, tw, tc, depth, ks, vec, mfma == 3, a);
         g.threads = c.threads;
         g.grid = c.grid;
         g.lds_bytes = int(std::min<int64_t>(c.lds, INT32_MAX));

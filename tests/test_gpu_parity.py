@@ -232,17 +232,16 @@ BAND_CASES = [
 
 @pytest.mark.parametrize("name,sh", BAND_CASES, ids=[c[0] for c in BAND_CASES])
 def test_parity_band_tiles(torch_dev, lib, name, sh):
-    """mfma = 2 band tiles (tw >= Q: runs of consecutive output pixels across
-    rows and images): small-integer inputs, so every schedule must match the
-    oracle exactly; every output written and nothing past the end.  Half the
-    points also run on operands 4 bytes past a 16-byte boundary."""
+    """mfma = 3 band tiles (runs of consecutive output pixels across rows and
+    images): small-integer inputs, so every schedule must match the oracle
+    exactly; every output written and nothing past the end.  Half the points
+    also run on operands 4 bytes past a 16-byte boundary."""
     torch = torch_dev
     x, w = synthdata.conv_inputs(sh, "int")
     ref = ok.conv2d_f64(x, w, sh).ravel()
     r = Runner(torch_dev, lib, 1, sh, x, w)
     o = osp.Space(1, sh)
-    Q = osp.conv_out(sh)[1]
-    pts = [p for p in o.valid_points() if o.knobs(p)["mfma"] == 2 and o.knobs(p)["tw"] >= Q]
+    pts = [p for p in o.valid_points() if o.knobs(p)["mfma"] == 3]
     assert pts
     rng = np.random.default_rng(zlib.crc32(name.encode()) % 1000)
     if len(pts) > 120:
@@ -295,7 +294,7 @@ MODEL_SCHEDULES = [
     dict(tk=8, th=4, tw=8, tc=8, unroll=16, lds=1, ks=1, mfma=0, vec=1),
     dict(tk=16, th=8, tw=8, tc=4, unroll=0, lds=0, ks=1, mfma=1, vec=1),
     dict(tk=64, th=8, tw=32, tc=16, unroll=512, lds=1, ks=1, mfma=2, vec=4),
-    dict(tk=64, th=4, tw=64, tc=8, unroll=16, lds=1, ks=2, mfma=2, vec=4),
+    dict(tk=64, th=4, tw=64, tc=8, unroll=16, lds=1, ks=2, mfma=3, vec=4),
 ]
 
 

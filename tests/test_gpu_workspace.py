@@ -63,7 +63,7 @@ SPLIT_CASES = [
      dict(tk=16, th=4, tw=32, tc=16, unroll=0, lds=1, ks=4, mfma=1, vec=4)),
     # channel-quad family, band tiles, four splits across workgroups
     ((2, 32, 14, 14, 64, 3, 3, 1, 1),
-     dict(tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=4, mfma=2, vec=4)),
+     dict(tk=32, th=4, tw=16, tc=4, unroll=0, lds=1, ks=4, mfma=3, vec=4)),
     # rectangular tiles, two wave groups and two splits across workgroups
     ((1, 64, 40, 40, 64, 3, 3, 1, 1),
      dict(tk=16, th=4, tw=16, tc=8, unroll=0, lds=1, ks=4, mfma=2, vec=4)),

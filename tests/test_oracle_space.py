@@ -54,10 +54,11 @@ def test_value_lists_named_shapes():
     s0 = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
     assert s0.values[0] == [1, 2, 4, 8, 16, 32, 64]
     # P = Q = 56: tile heights and widths up to 32, and 64 that covers a row
+    # (for band tiles)
     assert s0.values[1] == [1, 2, 4, 8, 16, 32, 64] == s0.values[2]
     assert s0.values[3] == [1, 2, 4, 8, 16, 32, 64]
-    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1, 2], [1, 4]]
-    assert s0.size() == 7 * 7 * 7 * 7 * 4 * 2 * 4 * 3 * 2
+    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1, 2, 3], [1, 4]]
+    assert s0.size() == 7 * 7 * 7 * 7 * 4 * 2 * 4 * 4 * 2
     s14 = sp.Space(sp.OP_CONV, (16, 512, 14, 14, 512, 3, 3, 1, 1))
     assert s14.values[1] == [1, 2, 4, 8, 16] == s14.values[2]
     s32 = sp.Space(sp.OP_CONV, (1, 8, 32, 32, 16, 3, 3, 1, 1))
@@ -177,7 +178,8 @@ def test_conv_mfma_small_tile_geometry():
 
 
 def test_conv_quad_geometry_hand_computed():
-    """mfma = 2 (channel-quad steps), worked by hand from the layout rules."""
+    """mfma = 2 (channel-quad steps, rectangular tiles) and mfma = 3 (the same
+    over band tiles), worked by hand from the layout rules."""
     s = sp.Space(sp.OP_CONV, (1, 64, 56, 56, 64, 3, 3, 1, 1))
     # 64 pixels over four waves, one 16x16 block each; unroll 64 over one
     # block -> u = 16 -> depth 3 -> 4 quads per step.  All 64 channels in one
@@ -186,11 +188,29 @@ def test_conv_quad_geometry_hand_computed():
     # 15 + 3 + 3 -> 24), channel stride 144 (= 16 mod 32); weight rows of
     # 16 * 9 = 144 -> 145 (odd) * 4 = 580 floats.  One buffer of
     # 16 * 580 + 64 * 144 = 18496 floats.  Copy units per thread:
-    # 2320 / 512 and 2304 / 512 -> 5.
+    # 2320 / 512 and 2304 / 512 -> 5.  Grid 4 x 14 x 4 (16 columns cover 56
+    # as 64).
     g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=64, lds=1, ks=2, mfma=2, vec=4))
     assert g == dict(valid=True, grid=4 * 14 * 4, threads=512, lds_bytes=4 * 18496, acc=4,
                      unroll_eff=3, t0=1, t1=1, red=576, chunks=1)
-    # the same tile with unroll 0 (one quad per step) and ks = 4: four wave
+    # The same knobs as a band (mfma = 3): 64 consecutive pixels spanning at
+    # most 1 + ceil(63 / 56) = 3 rows of one image: 2 + 3 = 5 padded rows of
+    # 55 + 3 + 3 -> 64 floats (aligned), channel stride 320 -> 336.  One buffer
+    # of 16 * 580 + 64 * 336 = 30784 floats; copy units 2320 / 512 -> 5 and
+    # 16 * 336 / 512 -> 11.  Grid 4 x ceil(3136 / 64): no padded pixel.
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=64, lds=1, ks=2, mfma=3, vec=4))
+    assert g == dict(valid=True, grid=4 * 49, threads=512, lds_bytes=4 * 30784, acc=4,
+                     unroll_eff=3, t0=1, t1=1, red=576, chunks=1)
+    # 4 x 8 tiles with 32-channel chunks: two waves of one block, 8 quads, two
+    # chunks and two buffers; ks = 2 -> two wave groups (8 % (2 * 4) == 0, 256
+    # threads).  Halo 6 rows of 7 + 3 = 10 (8 columns: no aligned layout),
+    # channel stride 60 -> 80; weight rows 32 * 9 = 288 -> 72 (even) -> 73 * 4
+    # = 292.  Buffer 16 * 292 + 32 * 80 = 7232 floats; copy units 1168 / 256
+    # -> 5 and (4-byte halo copies) 2560 / 256 -> 10.  Grid 4 * 14 * 7.
+    g = s.geometry(idx_of(s, tk=16, th=4, tw=8, tc=32, unroll=64, lds=1, ks=2, mfma=2, vec=4))
+    assert g == dict(valid=True, grid=4 * 14 * 7, threads=256, lds_bytes=4 * 2 * 7232, acc=4,
+                     unroll_eff=3, t0=1, t1=1, red=288, chunks=2)
+    # the 4 x 16 tile with unroll 0 (one quad per step) and ks = 4: four wave
     # groups of four waves, 64 * 4 * 4 = 1024 threads
     g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
     assert g["valid"] and g["threads"] == 1024 and g["grid"] == 224
@@ -207,6 +227,9 @@ def test_conv_quad_geometry_hand_computed():
     # blocks do not fit, 2 x 2 do)
     assert not s.valid(idx_of(s, tk=64, th=8, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
     assert s.valid(idx_of(s, tk=32, th=8, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
+    # rectangular tiles stay inside the output: 64 columns on 56 are bands only
+    assert not s.valid(idx_of(s, tk=16, th=1, tw=64, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
+    assert s.valid(idx_of(s, tk=16, th=1, tw=64, tc=64, unroll=0, lds=1, ks=4, mfma=3, vec=4))
     # The 3-channel stem: tc = 1 stands for the single chunk of all three
     # channels (one quad, channel 3 zero); 256 pixels -> four blocks per wave;
     # halo 7 * 2 + 7 = 21 rows of 31 * 2 + 7 + 3 -> 72 (aligned), channel
@@ -217,13 +240,19 @@ def test_conv_quad_geometry_hand_computed():
     g = st.geometry(idx_of(st, tk=16, th=8, tw=32, tc=1, unroll=0, lds=1, ks=1, mfma=2, vec=4))
     assert g == dict(valid=True, grid=4 * 14 * 4, threads=256, lds_bytes=4 * (16 * 198 + 4 * 1520),
                      acc=16, unroll_eff=1, t0=1, t1=4, red=196, chunks=1)
+    # the same knobs as a band: 256 pixels spanning at most 1 + ceil(255 /
+    # 112) = 4 rows: 3 * 2 + 7 = 13 padded rows of 111 * 2 + 7 + 3 -> 232
+    # floats, channel stride 3016 -> 3024; grid 4 x ceil(12544 / 256)
+    g = st.geometry(idx_of(st, tk=16, th=8, tw=32, tc=1, unroll=0, lds=1, ks=1, mfma=3, vec=4))
+    assert g == dict(valid=True, grid=4 * 49, threads=256, lds_bytes=4 * (16 * 198 + 4 * 3024),
+                     acc=16, unroll_eff=1, t0=1, t1=4, red=196, chunks=1)
     assert not st.valid(idx_of(st, tk=16, th=8, tw=32, tc=2, unroll=0, lds=1, ks=1, mfma=2, vec=4))
 
 
 def test_conv_band_geometry_hand_computed():
-    """mfma = 2 band tiles (tw >= Q), worked by hand."""
-    # VGG-16 L11 (16 images of 512 x 14 x 14): tw = 16 covers a row, so a
-    # tile is a band of 8 * 16 = 128 consecutive output pixels.  Four waves
+    """mfma = 3 band tiles, worked by hand."""
+    # VGG-16 L11 (16 images of 512 x 14 x 14): a band of 8 * 16 = 128
+    # consecutive output pixels.  Four waves
     # of two 16-pixel blocks, four channel blocks; 8-channel chunks: 2 quads,
     # 64 chunks, two buffers.  A band spans at most 1 + ceil(127 / 14) = 11
     # output rows with at most one image boundary among them: 10 + 1 * 2 + 3
@@ -233,12 +262,16 @@ def test_conv_band_geometry_hand_computed():
     # 8 * 240 = 6784 floats; copy units per thread: 1216 / 256 -> 5 and
     # 1920 / 256 -> 8.  Grid: 8 channel tiles x ceil(3136 / 128) = 25 bands.
     v = sp.Space(sp.OP_CONV, (16, 512, 14, 14, 512, 3, 3, 1, 1))
-    g = v.geometry(idx_of(v, tk=64, th=8, tw=16, tc=8, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    g = v.geometry(idx_of(v, tk=64, th=8, tw=16, tc=8, unroll=0, lds=1, ks=1, mfma=3, vec=4))
     assert g == dict(valid=True, grid=200, threads=256, lds_bytes=4 * 2 * 6784, acc=32,
                      unroll_eff=1, t0=4, t1=2, red=72, chunks=64)
-    # tiles past the height are bands only; the other families have no such
-    # tiles at all
+    # a band depends on th * tw only: 16 x 8 is the same 128-pixel band
+    g16 = v.geometry(idx_of(v, tk=64, th=16, tw=8, tc=8, unroll=0, lds=1, ks=1, mfma=3, vec=4))
+    assert g16 == g
+    # as rectangles, neither fits inside 14 x 14
+    assert not v.valid(idx_of(v, tk=64, th=8, tw=16, tc=8, unroll=0, lds=1, ks=1, mfma=2, vec=4))
     assert not v.valid(idx_of(v, tk=64, th=16, tw=8, tc=8, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    # the other families have no tiles past the output at all
     g = v.geometry(idx_of(v, tk=64, th=8, tw=16, tc=8, unroll=0, lds=1, ks=1, mfma=1, vec=4))
     assert g == dict(valid=False, grid=0, threads=0, lds_bytes=0, acc=0, unroll_eff=1, t0=0,
                      t1=0, red=0, chunks=0)
@@ -250,7 +283,7 @@ def test_conv_band_geometry_hand_computed():
     # thread: 160 / 256 -> 1 and 4 * 688 / 256 -> 11.  Buffer 32 * 20 +
     # 16 * 688 = 11648 floats, two of them; grid 16 x ceil(784 / 128) = 7.
     r = sp.Space(sp.OP_CONV, (1, 256, 56, 56, 512, 1, 1, 2, 0))
-    g = r.geometry(idx_of(r, tk=32, th=4, tw=32, tc=16, unroll=0, lds=1, ks=1, mfma=2, vec=4))
+    g = r.geometry(idx_of(r, tk=32, th=4, tw=32, tc=16, unroll=0, lds=1, ks=1, mfma=3, vec=4))
     assert g == dict(valid=True, grid=112, threads=256, lds_bytes=4 * 2 * 11648, acc=16,
                      unroll_eff=1, t0=2, t1=2, red=16, chunks=16)
 
