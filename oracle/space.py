@@ -349,7 +349,8 @@ def conv_quad_geometry(shape, v):
     4 * quads * R * S with 16-byte weight copies, else the smallest 2 * odd)
     and 4 * quads halo channels of cs floats (the smallest >= hs * ws that is
     16 mod 32); two buffers when a workgroup walks more than one chunk; the
-    wave groups' partial tiles reuse it.  Validity adds: at least one 16x16
+    wave groups' partial tiles and the output staging rows (16 x 68 floats
+    per pixel wave) reuse it.  Validity adds: at least one 16x16
     block, chunks of whole channel quads (tc >= 4, or tc = 1 standing for all
     channels of an image with fewer than four), LDS staging, the register
     budget of the compiled instances (at most 32, 16, 4 blocks per wave and
@@ -408,7 +409,9 @@ def conv_quad_geometry(shape, v):
     ok = ok and (C < 4 or per_thread <= 12)
     nbuf = 2 if cps > 1 else 1
     buf = tk * wrow + 4 * quads * cs
-    lds = max(4 * nbuf * buf, 16 * (kg - 1) * waves * 64 * blocks)
+    # buffers; the wave groups' partial tiles; the output staging rows (16
+    # rows of 68 floats per pixel wave)
+    lds = max(4 * nbuf * buf, 16 * (kg - 1) * waves * 64 * blocks, 4 * 16 * 68 * waves)
     if band:
         grid = ksw * _cdiv(K, tk) * _cdiv(N * P * Q, npx)
         images = min(N, 1 + _cdiv(npx - 1, P * Q))

@@ -143,6 +143,9 @@ struct Conv2Args {
     int hp;               // band tiles: padded rows per image, (P - 1) * st + R; image n's
                           //    output row p reads padded rows n * hp + p * st + r
     int F;                // band tiles: N * P * Q
+    int st4;              // output stores of 4 consecutive pixels are 16-byte aligned (y and
+                          //    partials 16-byte aligned; P*Q, and for rectangles Q and tw,
+                          //    multiples of 4)
     int chunks, cps;      // reduction chunks, chunks per split
     int t4;               // channel quads per chunk (channel slots / 4)
     int hs, ws, cs;       // halo rows, halo row stride, halo channel stride (floats)
@@ -161,7 +164,7 @@ struct Conv2Args {
     int w_dk, w_dc;       // blockDim in (weight row, unit) mixed radix
     int h_dc, h_dr;       // blockDim in (halo channel, unit) mixed radix
     FastDiv f_wru, f_hcu, f_hru, f_rs, f_s, f_tk, f_tq, f_tp, f_ksw;
-    FastDiv f_q, f_p, f_hp;   // band tiles: Q, P, hp
+    FastDiv f_q, f_p, f_hp, f_pq;   // band tiles: Q, P, hp, P*Q
 };
 
 // Launch shape of a conv_mfma2 point.
@@ -313,7 +316,13 @@ inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc,
     a.f_tk = make_fastdiv(a.tiles_k); a.f_tq = make_fastdiv(std::max(1, a.tiles_q));
     a.f_tp = make_fastdiv(a.tiles_p); a.f_ksw = make_fastdiv(a.ksw);
     a.f_q = make_fastdiv(a.Q); a.f_p = make_fastdiv(a.P); a.f_hp = make_fastdiv(std::max(1, a.hp));
-    g.lds = std::max<int64_t>(4 * int64_t(a.nbuf) * buf, int64_t(16) * (kg - 1) * a.wpx * 64 * body);
+    a.f_pq = make_fastdiv(std::max(1, a.P * a.Q));
+    a.st4 = band ? (int64_t(a.P) * a.Q) % 4 == 0 : a.Q % 4 == 0 && tw % 4 == 0;
+    // buffers; the wave groups' partial tiles; the output staging rows (16
+    // rows of 68 floats per pixel wave)
+    g.lds = std::max<int64_t>({4 * int64_t(a.nbuf) * buf,
+                               int64_t(16) * (kg - 1) * a.wpx * 64 * body,
+                               int64_t(4) * 16 * 68 * a.wpx});
     g.grid = grid;
     g.red = tc4 * RS;
     g.valid = ok && g.lds <= kLdsLimit && g.threads <= kThreadsLimit && g.grid <= kGridLimit;

@@ -501,6 +501,9 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         if (reinterpret_cast<uintptr_t>(w) % 16 != 0) a.vw = 0;
         if (reinterpret_cast<uintptr_t>(x) % 16 != 0) a.vh = 0;
         if (a.vw != vw0 || a.vh != vh0) conv2_units(a, c.threads);
+        // 16-byte output stores only into a 16-byte aligned output (and
+        // partials: the workspace is)
+        if (reinterpret_cast<uintptr_t>(y) % 16 != 0) a.st4 = 0;
         plan.func = conv_mfma2_instance(c.tkb, c.npb, c.u, c.kg);
         plan.family = DS_KERNEL_CONV_MFMA2;
         plan.nparams = 4;

@@ -1064,27 +1064,74 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
                 for (int b = 0; b < NPB; ++b) dst[(i * NPB + b) * 64 + lane] = acc[i][b];
         }
         __syncthreads();
-        if (g > 0) return;
+        if (g == 0) {
 #pragma unroll
-        for (int h = 1; h < KG; ++h) {
-            const floatx4 *src = red + ((h - 1) * a.wpx + wp) * per_wave;
+            for (int h = 1; h < KG; ++h) {
+                const floatx4 *src = red + ((h - 1) * a.wpx + wp) * per_wave;
 #pragma unroll
-            for (int i = 0; i < TKB; ++i)
+                for (int i = 0; i < TKB; ++i)
 #pragma unroll
-                for (int b = 0; b < NPB; ++b) acc[i][b] += src[(i * NPB + b) * 64 + lane];
+                    for (int b = 0; b < NPB; ++b) acc[i][b] += src[(i * NPB + b) * 64 + lane];
+            }
         }
     }
-    // 16x16 block: lane holds rows 4*lg + v (channels), column li (pixel)
+    // Stores go through LDS: a 16x16 block leaves a lane one pixel of four
+    // channels, so each wave of group 0 writes 16 channels x up to 64 pixels
+    // at a time to its own LDS rows and reads them back as 4 consecutive
+    // pixels of one channel per lane -- 16-byte stores, runs of up to 256
+    // bytes per channel row.  The LDS is free once every wave is past its
+    // last operand (or reduction) read.
+    __syncthreads();
+    if (g > 0) return;
+    constexpr int BG = NPB < 4 ? NPB : 4;              // blocks per pass
+    constexpr int ROW = 16 * BG + 4;                    // staging row stride (floats)
+    constexpr int LPR = 4 * BG;                         // lanes per channel row
+    float *stage = smem + wp * (16 * 68);
     float *yn = (a.ksw > 1 ? a.part + (size_t)z * a.N * a.K * PQ : a.y) + (size_t)n * a.K * PQ;
+    auto put = [&](int k, int pix, floatx4 val) {
+        if (k >= a.K) return;
+        if (a.band) {
+            const int f = qt * a.npx + pix;
+            if (a.st4 && f + 3 < a.F) {
+                const int img = fdv(f, a.f_pq);
+                *reinterpret_cast<floatx4 *>(yn + (size_t)img * a.K * PQ + (size_t)k * PQ +
+                                             (f - img * PQ)) = val;
+                return;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int fe = f + e;
+                if (fe >= a.F) break;
+                const int img = fdv(fe, a.f_pq);
+                yn[(size_t)img * a.K * PQ + (size_t)k * PQ + (fe - img * PQ)] = val[e];
+            }
+        } else {
+            const int py = pix >> a.ltw, px = pix & (a.tw - 1);
+            const int p = pt * a.th + py, q = qt * a.tw + px;
+            if (a.st4 && p < a.P && q + 3 < a.Q) {
+                *reinterpret_cast<floatx4 *>(yn + (size_t)k * PQ + p * a.Q + q) = val;
+                return;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int pe = pt * a.th + ((pix + e) >> a.ltw), qe = qt * a.tw + ((pix + e) & (a.tw - 1));
+                if (pe < a.P && qe < a.Q) yn[(size_t)k * PQ + pe * a.Q + qe] = val[e];
+            }
+        }
+    };
 #pragma unroll
     for (int i = 0; i < TKB; ++i)
 #pragma unroll
-        for (int b = 0; b < NPB; ++b) {
-            if (!pv[b]) continue;
+        for (int b0 = 0; b0 < NPB; b0 += BG) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int k = kt * a.tk + i * 16 + 4 * lg + v;
-                if (k < a.K) yn[(size_t)k * PQ + oq[b]] = acc[i][b][v];
+            for (int bb = 0; bb < BG; ++bb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) stage[(4 * lg + v) * ROW + bb * 16 + li] = acc[i][b0 + bb][v];
+#pragma unroll
+            for (int r0 = 0; r0 < 16; r0 += 64 / LPR) {
+                const int row = r0 + lane / LPR, c4 = lane % LPR;
+                const floatx4 val = *reinterpret_cast<const floatx4 *>(stage + row * ROW + 4 * c4);
+                put(kt * a.tk + i * 16 + row, (wp * NPB + b0) * 16 + 4 * c4, val);
             }
         }
 }
