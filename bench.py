@@ -351,7 +351,18 @@ def main(argv=None):
                     "achieved": round(ach / 1e12, 3), "peak": PEAK_FP32_TFLOPS,
                     "unit": "TFLOP/s"}
     roofline["frac"] = round(roofline["achieved"] / roofline["peak"], 4)
-    roofline.update({"traffic": measured_traffic(task["kernel"], task["knobs"], task["shape"]),
+    # A split schedule is two launches per layer (the kernel, then the reduce
+    # of its partial outputs): the events time both, and so does the traffic.
+    splits = task["space"].kernel_info(task["best"].index())["splits"]
+    traffic = measured_traffic(task["kernel"], task["knobs"], task["shape"])
+    if splits > 1:
+        red = f"split_reduce_kernel<{splits}>"
+        n4 = -(-int(task["yd"].numel()) // 4)          # the reduce's launch: float4 lanes,
+        roofline.update({"reduce_kernel": red,         # 256-thread blocks, at most 4096
+                         "reduce_grid_threads": min(-(-n4 // 256), 4096) * 256})
+        rt = measured_traffic(red, task["knobs"], task["shape"])
+        traffic = traffic + rt if traffic is not None and rt is not None else None
+    roofline.update({"traffic": traffic,
                      "kernel": task["kernel"], "task": task["name"],
                      "schedule": task["knobs"],
                      "grid_threads": int(task["geom"]["grid"]) * int(task["geom"]["threads"]),

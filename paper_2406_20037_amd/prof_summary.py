@@ -23,6 +23,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = {
     "mm_": ["csrc/kern_matmul.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
     "conv_": ["csrc/kern_conv.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
+    "split_reduce_kernel": ["csrc/harness.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
 }
 
 
@@ -66,7 +67,7 @@ def traffic_key(kernel: str, sched: str, shape=None) -> str:
 def short(name: str) -> str:
     return (name.replace("ds::(anonymous namespace)::", "").replace("void ", "")
             .replace("(ds::MatmulArgs)", "").replace("(ds::ConvArgs)", "")
-            .replace("(ds::Conv2Args)", ""))
+            .replace("(ds::Conv2Args)", "").replace("(float const*, float*, long)", ""))
 
 
 def top_kernels(db, top):
@@ -95,12 +96,14 @@ def bench_check(db, bench_json):
         line = [ln for ln in fh if ln.lstrip().startswith("{")][-1]
     rf = json.loads(line)["roofline"]
     kname, threads = rf["kernel"], rf.get("grid_threads")
+    red, rgrid = rf.get("reduce_kernel"), rf.get("reduce_grid_threads")
     cur = sqlite3.connect(db).cursor()
-    durs = [(d, g) for name, d, g in cur.execute(
-        "select name, duration, grid_x * grid_y * grid_z from kernels") if short(name) == kname]
+    rows = list(cur.execute("select name, duration, grid_x * grid_y * grid_z from kernels"))
+    durs = [(d, g) for name, d, g in rows if short(name) == kname]
     at = sorted(d for d, g in durs if threads is None or g == threads)
     print(f"\n### Dominant kernel of the profiled bench.py run\n")
-    print(f"bench.py: `{kname}` on task {rf['task']}, average launch {rf['avg_launch_us']:.3f} us "
+    what = f"`{kname}`" + (f" followed by `{red}`" if red else "")
+    print(f"bench.py: {what} on task {rf['task']}, average launch {rf['avg_launch_us']:.3f} us "
           f"(events around its launches in the timed passes), {rf['achieved']} {rf['unit']} "
           f"= {rf['frac']:.3f} of {rf['peak']}.\n")
     if not at:
@@ -108,11 +111,22 @@ def bench_check(db, bench_json):
         return
     mean = sum(at) / len(at) / 1e3
     med = at[len(at) // 2] / 1e3
-    print("| dispatches (this instance, this grid) | mean us | median us | min us | bench avg launch us "
-          "| bench - trace mean us |")
-    print("|---:|---:|---:|---:|---:|---:|")
-    print(f"| {len(at)} of {len(durs)} | {mean:.3f} | {med:.3f} | {at[0] / 1e3:.3f} | "
-          f"{rf['avg_launch_us']:.3f} | {rf['avg_launch_us'] - mean:.3f} |")
+    print("| kernel | dispatches (this instance, this grid) | mean us | median us | min us |")
+    print("|---|---:|---:|---:|---:|")
+    print(f"| `{kname}` | {len(at)} of {len(durs)} | {mean:.3f} | {med:.3f} | {at[0] / 1e3:.3f} |")
+    total = med
+    if red:
+        # (every split schedule of this split count and output-size class
+        # launches the same reduce grid; its median is the common case)
+        rd = sorted(d for name, d, g in rows if short(name) == red and (rgrid is None or g == rgrid))
+        if rd:
+            rmed = rd[len(rd) // 2] / 1e3
+            total += rmed
+            print(f"| `{red}` | {len(rd)} | {sum(rd) / len(rd) / 1e3:.3f} | {rmed:.3f} | "
+                  f"{rd[0] / 1e3:.3f} |")
+    print(f"\nTraced median per layer launch {total:.3f} us against the bench's "
+          f"{rf['avg_launch_us']:.3f} us (difference {rf['avg_launch_us'] - total:.3f} us, "
+          f"{(rf['avg_launch_us'] - total) / total * 100:+.1f}%).")
 
 
 def main(argv=None):
