@@ -1,9 +1,9 @@
 /*
  * droplet.h -- C ABI of the MI355X (gfx950) schedule-tuning library.
  *
- * The library implements the hot path of the combined explore/exploit kernel
- * scheduler of "Explore as a Storm, Exploit as a Raindrop" (Canesche, Verma,
- * Pereira): a schedule-parameterised fp32 kernel family (NCHW conv2d and
+ * The library implements the measurement-driven core of the combined
+ * explore/exploit kernel scheduler of "Explore as a Storm, Exploit as a
+ * Raindrop" (Canesche, Verma, Pereira): a schedule-parameterised fp32 kernel family (NCHW conv2d and
  * row-major matmul) written in HIP for gfx950, a hipEvent measurement harness,
  * a seeded exploration sampler and Droplet Search coordinate descent.
  *
@@ -110,10 +110,15 @@ int sched_space_info(const ds_space *space, int *op, int *nknobs, uint64_t *size
 int sched_space_axis(const ds_space *space, int axis, const char **name, int *nvalues,
                      const int32_t **values);
 
-/* 1 if s is a valid point of the space, 0 if not, < 0 on a bad argument. */
+/* 1 if s is a valid point of the space, 0 if not, < 0 on a bad argument.  The
+ * search space of a sketch is the set of its valid annotations (Definition 1);
+ * Section 3 (RQ4) notes that some annotations give kernels that cannot run,
+ * which is what this predicate excludes. */
 int sched_valid(const ds_space *space, const ds_sched *s);
 
-/* Mixed-radix key: sum over axes of idx[a] * prod_{b<a} nvalues[b]. */
+/* Mixed-radix key of a point of the lattice whose coordinates are the knob
+ * indices (Section 2.2, Example 3): sum over axes of idx[a] * prod_{b<a}
+ * nvalues[b]. */
 int sched_key(const ds_space *space, const ds_sched *s, uint64_t *key);
 int sched_from_key(const ds_space *space, uint64_t key, ds_sched *out);
 
@@ -300,7 +305,9 @@ typedef struct {
 } ds_tune_io;
 
 /*
- * ds_measure -- a5 of the hot path: parity-check the first launch (y is
+ * ds_measure -- one trial, the observed execution of a concrete schedule
+ * (Section 2.1, "Termination in Ansor"; each search step of Section 2.2 is
+ * such a measurement): parity-check the first launch (y is
  * pre-filled with NaN; the check fails on NaN/Inf or max|y-ref| > tol*max|ref|),
  * warm up, then time cfg->repeat repeats of `number` launches between two
  * hipEvents on io->stream.  Synchronises the stream.  best_so_far_ms (0 = none)
