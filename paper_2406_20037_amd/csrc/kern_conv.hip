@@ -794,8 +794,34 @@ __device__ __forceinline__ void copy(const char *base, unsigned off, float *dst)
 
 }  // namespace q4
 
+// Waves per SIMD each conv_mfma2 instance is compiled to allow: the most of
+// 4 and 3 for which its registers fit without spilling (found by compiling
+// every instance under each bound); others keep the compiler's choice.  On
+// its own the compiler keeps the accumulators in AGPRs beside the VGPRs and
+// ends at fewer waves: conv_mfma2<4, 4, 1, 1>, for one, takes 164 VGPRs + 64
+// AGPRs (2 waves) unbounded and 152 VGPRs (3 waves) bounded.  An instance is
+// keyed TKB·10000 + NPB·100 + U·10 + KG.
+constexpr int kConv2Waves4[] = {
+    10111, 10112, 10114, 10121, 10122, 10124, 10141, 10142, 10144, 10211, 10212, 10214,
+    10221, 10222, 10224, 10241, 10242, 10244, 10411, 10412, 10414, 10421, 10422, 10424,
+    10441, 10442, 10444, 10811, 10812, 20111, 20112, 20114, 20121, 20122, 20124, 20141,
+    20142, 20144, 20211, 20212, 20214, 20221, 20222, 20224, 20241, 20242, 20244, 20411,
+    20412, 40111, 40112, 40114, 40121, 40122, 40124, 40141, 40142, 40144, 40211, 40212,
+    40221, 40222};
+constexpr int kConv2Waves3[] = {
+    10821, 10822, 10841, 10842, 20421, 20422, 20441, 20442, 20811, 20812, 40241, 40242,
+    40411, 40412};
+constexpr int conv2_waves(int tkb, int npb, int u, int kg) {
+    const int key = tkb * 10000 + npb * 100 + u * 10 + kg;
+    for (int k : kConv2Waves4)
+        if (k == key) return 4;
+    for (int k : kConv2Waves3)
+        if (k == key) return 3;
+    return 1;
+}
+
 template <int TKB, int NPB, int U, int KG>
-__global__ __launch_bounds__(256 * KG) void conv_mfma2(Conv2Args a) {
+__global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_mfma2(Conv2Args a) {
     extern __shared__ float smem[];
     using q4::fdv;
     // tile of this workgroup (tile order: k, q, p, split, image)
