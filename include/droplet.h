@@ -69,17 +69,19 @@ typedef struct ds_space ds_space;
  * sched_space_create -- the kernel search space of one kernel family at one
  * shape (Definition 1).  conv2d axes, in order: tk, th, tw, tc (powers of two
  * 1..64 kept if <= K, P, Q, C; th and tw also keep the smallest power of two
- * >= P, Q), unroll {0,16,64,512}, lds {0,1}, ks {1,2,4,8} (kept if <= C),
- * mfma {0,1,2,3}, vec {1,4} (floats per lane of the global -> LDS copies).
+ * >= P, Q), unroll {0,16,64,512}, lds {0,1}, ks {1,2,4,...,32} (kept if
+ * <= C), mfma {0,1,2,3}, vec {1,4} (floats per lane of the global -> LDS
+ * copies).
  * conv mfma: 0 VALU FMA; 1 fp32 MFMA over 16-step groups of the (c, r, s)
  * reduction (a per-chunk offset table locates each tap); 2 fp32 MFMA over
  * (tap, channel quad) steps, LDS staging only, where ks first splits every
  * chunk's quads between up to four wave groups of one workgroup (summed in
  * LDS) and the rest across workgroups; 3 the same over band tiles: th * tw
  * consecutive pixels of the output flattened over (image, row, column).  Only
- * band tiles may reach past the output's height or width.  matmul axes: bm, bn {16,...,256} (kept if <= M, N),
- * bk {4,...,64} (kept if <= K), unroll, dbuf {0,1}, mfma {0,1}, ks {1,2,4,8}
- * (kept if <= K), vec {1,4} (floats per lane of the operand loads).  The
+ * band tiles may reach past the output's height or width.  matmul axes: bm,
+ * bn {16,...,256} (kept if <= M, N), bk {4,...,64} (kept if <= K), unroll,
+ * dbuf {0,1}, mfma {0,1}, ks {1,2,4,8} (kept if <= K), vec {1,4} (floats per
+ * lane of the operand loads).  The
  * smallest value of a clipped axis is always kept.  A point is valid when its
  * kernel fits the hardware (threads, LDS, workgroups) and the register budget
  * of its compiled instance (no spill), and, for vec 4, an operand can move 16

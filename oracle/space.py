@@ -19,7 +19,8 @@ conv2d (op 1), shape (N, C, H, W, K, R, S, stride, pad), axes in order
         value >= P, Q (only band tiles, mfma 3, may reach past the output);
     unroll in {0, 16, 64, 512}: maximum unrolled steps of the reduction loop;
     lds in {0, 1}: stage input and weight tiles in LDS;
-    ks in {1, 2, 4, 8}: reduction split over C across workgroups (kept if <= C);
+    ks in {1, 2, 4, 8, 16, 32}: reduction split over C across workgroups (kept
+        if <= C);
     mfma in {0, 1, 2, 3}: contract on VALU FMA (0) or fp32 MFMA (implicit
         GEMM): 1 steps through 16-step groups of the (c, r, s) reduction, 2
         through (tap, channel quad) steps over rectangular tiles (a second MFMA
@@ -72,6 +73,7 @@ GRID_LIMIT = 2 ** 31 - 1
 POW2_64 = [1, 2, 4, 8, 16, 32, 64]
 UNROLL = [0, 16, 64, 512]
 SPLITK = [1, 2, 4, 8]
+CONV_SPLIT = [1, 2, 4, 8, 16, 32]
 MM_TILE = [16, 32, 64, 128, 256]
 MM_BK = [4, 8, 16, 32, 64]
 
@@ -217,7 +219,7 @@ class Space(Lattice):
             P, Q = conv_out(shape)
             values = [
                 _clip(POW2_64, K), _cover(POW2_64, P), _cover(POW2_64, Q), _clip(POW2_64, C),
-                list(UNROLL), [0, 1], _clip(SPLITK, C), [0, 1, 2, 3], list(VEC),
+                list(UNROLL), [0, 1], _clip(CONV_SPLIT, C), [0, 1, 2, 3], list(VEC),
             ]
             names = CONV_AXES
         else:

@@ -1,6 +1,7 @@
 // Launch plans, kernel_run, reference kernels and the hipEvent measurement
 // harness (the "trial" of Section 2.1: observing one schedule's execution).
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstring>
 #include <limits>
@@ -88,6 +89,17 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float *__restri
         }
     }
 }
+
+constexpr int kMaxSplits = 32;
+
+template <int... S>
+constexpr std::array<const void *, sizeof...(S) + 2> split_reduce_table(
+    std::integer_sequence<int, S...>) {
+    return {nullptr, nullptr, reinterpret_cast<const void *>(&split_reduce_kernel<S + 2>)...};
+}
+// kSplitReduce[S]: the reduce kernel of S partial slices, 2 <= S <= kMaxSplits
+const std::array<const void *, kMaxSplits + 1> kSplitReduce =
+    split_reduce_table(std::make_integer_sequence<int, kMaxSplits - 1>{});
 
 __global__ void fill_u32_kernel(unsigned *p, int n) {
     if (int(threadIdx.x) < n) p[threadIdx.x] = 0u;
@@ -646,8 +658,8 @@ int fill_async(float *p, int64_t n, float v, hipStream_t stream) {
 
 int launch_plan(const Plan &plan, hipStream_t stream) {
     if (plan.grid == 0 || plan.y_elems == 0) return DS_OK;
-    if (plan.splits > 8) {      // the lattice's split axis stops at 8
-        set_error("more than 8 reduction splits");
+    if (plan.splits > kMaxSplits) {      // the lattice's split axes stop at 32
+        set_error("more than %d reduction splits", kMaxSplits);
         return DS_EUNSUPPORTED;
     }
     int rc = ensure_lds_attr(plan.func, plan.lds);
@@ -667,18 +679,10 @@ int launch_plan(const Plan &plan, hipStream_t stream) {
                                : plan.op == DS_OP_CONV2D_NCHW ? plan.conv.part : plan.mm.part;
         const int64_t n4 = cdiv64(plan.y_elems, 4);
         const int64_t blocks = std::min<int64_t>(cdiv64(n4, 256), 4096);
-        const void *reduce[] = {nullptr, nullptr,
-                                reinterpret_cast<const void *>(&split_reduce_kernel<2>),
-                                reinterpret_cast<const void *>(&split_reduce_kernel<3>),
-                                reinterpret_cast<const void *>(&split_reduce_kernel<4>),
-                                reinterpret_cast<const void *>(&split_reduce_kernel<5>),
-                                reinterpret_cast<const void *>(&split_reduce_kernel<6>),
-                                reinterpret_cast<const void *>(&split_reduce_kernel<7>),
-                                reinterpret_cast<const void *>(&split_reduce_kernel<8>)};
         int64_t n = plan.y_elems;
         void *rargs[] = {const_cast<float **>(&part), &y, &n};
-        if (!hip_ok(hipLaunchKernel(reduce[plan.splits], dim3(unsigned(blocks)), dim3(256), rargs, 0,
-                                    stream),
+        if (!hip_ok(hipLaunchKernel(kSplitReduce[plan.splits], dim3(unsigned(blocks)), dim3(256),
+                                    rargs, 0, stream),
                     "split reduce launch"))
             return DS_EHIP;
         if (!hip_ok(hipGetLastError(), "split reduce launch")) return DS_EHIP;

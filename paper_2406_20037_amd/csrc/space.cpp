@@ -18,6 +18,9 @@ thread_local std::string g_error;
 const int32_t kPow2to64[] = {1, 2, 4, 8, 16, 32, 64};
 const int32_t kUnroll[] = {0, 16, 64, 512};
 const int32_t kSplit[] = {1, 2, 4, 8};
+// conv splits reach 32: a batch-1 layer with few output pixels fills the
+// chip only through its reduction
+const int32_t kConvSplit[] = {1, 2, 4, 8, 16, 32};
 const int32_t kMmTile[] = {16, 32, 64, 128, 256};
 const int32_t kMmBk[] = {4, 8, 16, 32, 64};
 const int32_t kOnOff[] = {0, 1};
@@ -342,7 +345,7 @@ int build_space(int op, const int64_t *sh, int shape_len, Space &sp) {
         for (int i = 0; i < 9; ++i) sp.shape[i] = sh[i];
         sp.values = {clipped(kPow2to64, K), covering(kPow2to64, P), covering(kPow2to64, Q),
                      clipped(kPow2to64, C), all_of(kUnroll), all_of(kOnOff),
-                     clipped(kSplit, C), all_of(kConvMfma),    all_of(kVec)};
+                     clipped(kConvSplit, C), all_of(kConvMfma), all_of(kVec)};
         sp.names.assign(kConvNames, kConvNames + 9);
     } else if (op == DS_OP_MATMUL_RM) {
         if (shape_len != 3) {

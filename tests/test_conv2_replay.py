@@ -15,7 +15,9 @@ oracle's hand-worked pins do not cover.
 Shapes: bands crossing image boundaries, several images per band, strides 2,
 3 input channels, no padding, 5x5 filters, W not a multiple of 4, ragged K.
 Points: sampled valid mfma 2 and 3 points of each shape; a third of them also
-replayed with both operands 4 bytes off a 16-byte boundary.
+replayed with both operands 4 bytes off a 16-byte boundary.  Split shapes:
+batch-1 layers with many channels and few output pixels, replayed at 16 and
+32 reduction splits only (including splits left empty by the chunk count).
 """
 import os
 import random
@@ -44,6 +46,11 @@ SHAPES = [
     (2, 4, 30, 30, 17, 5, 5, 1, 2),
 ]
 PER_SHAPE = 14
+SPLIT_SHAPES = [
+    (1, 128, 7, 7, 32, 3, 3, 1, 1),
+    (1, 256, 14, 14, 32, 3, 3, 2, 1),
+    (1, 96, 6, 6, 16, 1, 1, 1, 0),
+]
 
 
 @pytest.fixture(scope="module")
@@ -59,15 +66,7 @@ def replay_bin(tmp_path_factory):
     return out
 
 
-@pytest.mark.parametrize("sh", SHAPES, ids=["x".join(map(str, s)) for s in SHAPES])
-def test_conv2_index_replay(replay_bin, sh):
-    s = sp.Space(sp.OP_CONV, sh)
-    pts = [p for p in s.valid_points() if s.knobs(p)["mfma"] >= 2]
-    assert pts
-    rng = random.Random(hash(sh) & 0xFFFF)
-    band = [p for p in pts if s.knobs(p)["mfma"] == 3]
-    rect = [p for p in pts if s.knobs(p)["mfma"] == 2]
-    pick = rng.sample(band, min(PER_SHAPE, len(band))) + rng.sample(rect, min(PER_SHAPE // 2, len(rect)))
+def _replay(replay_bin, s, sh, pick):
     lines = []
     for i, p in enumerate(pick):
         v, g = s.knobs(p), s.geometry(p)
@@ -79,3 +78,25 @@ def test_conv2_index_replay(replay_bin, sh):
     out = r.stdout.strip().splitlines()
     assert r.returncode == 0 and len(out) == len(lines) and all(o.startswith("ok") for o in out), (
         f"{lines[len(out) - 1] if out else lines[0]}: {out[-1:] } {r.stderr[-2000:]}")
+
+
+@pytest.mark.parametrize("sh", SHAPES, ids=["x".join(map(str, s)) for s in SHAPES])
+def test_conv2_index_replay(replay_bin, sh):
+    s = sp.Space(sp.OP_CONV, sh)
+    pts = [p for p in s.valid_points() if s.knobs(p)["mfma"] >= 2]
+    assert pts
+    rng = random.Random(hash(sh) & 0xFFFF)
+    band = [p for p in pts if s.knobs(p)["mfma"] == 3]
+    rect = [p for p in pts if s.knobs(p)["mfma"] == 2]
+    pick = rng.sample(band, min(PER_SHAPE, len(band))) + rng.sample(rect, min(PER_SHAPE // 2, len(rect)))
+    _replay(replay_bin, s, sh, pick)
+
+
+@pytest.mark.parametrize("sh", SPLIT_SHAPES, ids=["x".join(map(str, s)) for s in SPLIT_SHAPES])
+def test_conv2_index_replay_many_splits(replay_bin, sh):
+    s = sp.Space(sp.OP_CONV, sh)
+    pts = [p for p in s.valid_points() if s.knobs(p)["mfma"] >= 2 and s.knobs(p)["ks"] >= 16]
+    # 96 channels make 24 quad chunks: 16 splits leave some empty, 32 are invalid
+    assert {s.knobs(p)["ks"] for p in pts} == ({16} if sh[1] == 96 else {16, 32})
+    rng = random.Random(hash(sh) & 0xFFFF)
+    _replay(replay_bin, s, sh, rng.sample(pts, min(PER_SHAPE, len(pts))))

@@ -95,6 +95,37 @@ def test_capture_after_the_workspace_exists(env, sh, knobs):
     del g
 
 
+MANY_SPLITS = [
+    # band tiles, 32 splits of 64 quad chunks (stride 2)
+    ((1, 256, 14, 14, 64, 3, 3, 2, 1),
+     dict(tk=16, th=2, tw=8, tc=4, unroll=0, lds=1, ks=32, mfma=3, vec=4)),
+    # rectangular tiles, 1x1 filter, 32 splits
+    ((1, 512, 7, 7, 64, 1, 1, 1, 0),
+     dict(tk=16, th=4, tw=4, tc=4, unroll=0, lds=1, ks=32, mfma=2, vec=4)),
+    # tabled MFMA family, 32 splits
+    ((1, 256, 14, 14, 64, 3, 3, 2, 1),
+     dict(tk=16, th=4, tw=4, tc=4, unroll=0, lds=1, ks=32, mfma=1, vec=4)),
+    # VALU family: 24 chunks over 16 splits leave 4 of them empty (12 partials)
+    ((1, 96, 7, 7, 32, 3, 3, 1, 1),
+     dict(tk=4, th=4, tw=4, tc=4, unroll=0, lds=1, ks=16, mfma=0, vec=4)),
+]
+
+
+@pytest.mark.parametrize("sh,knobs", MANY_SPLITS,
+                         ids=["band_ks32", "rect_ks32", "mfma1_ks32", "valu_ks16_empty"])
+def test_many_splits_match_the_oracle(env, sh, knobs):
+    """16 and 32 reduction splits (a reduce launch over as many partial
+    slices, empty splits skipped) agree with the fp64 oracle."""
+    torch, L = env
+    c = conv_case(torch, L, sh, knobs)
+    splits = L.Space(L.DS_OP_CONV2D_NCHW, sh).kernel_info(c["s"].index())["splits"]
+    assert splits == (12 if sh[1] == 96 else knobs["ks"])
+    print("many splits", sh, knobs, flush=True)
+    L.kernel_run(L.DS_OP_CONV2D_NCHW, c["s"], c["x"], c["w"], c["y"], torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    close(torch, c)
+
+
 def test_capture_without_a_workspace_is_refused(env):
     torch, L = env
     c = conv_case(torch, L, (1, 32, 20, 20, 32, 3, 3, 1, 1),

@@ -57,12 +57,15 @@ def test_value_lists_named_shapes():
     # (for band tiles)
     assert s0.values[1] == [1, 2, 4, 8, 16, 32, 64] == s0.values[2]
     assert s0.values[3] == [1, 2, 4, 8, 16, 32, 64]
-    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8], [0, 1, 2, 3], [1, 4]]
-    assert s0.size() == 7 * 7 * 7 * 7 * 4 * 2 * 4 * 4 * 2
+    # conv splits reach 32 (C = 64 keeps all six)
+    assert s0.values[4:] == [[0, 16, 64, 512], [0, 1], [1, 2, 4, 8, 16, 32], [0, 1, 2, 3],
+                             [1, 4]]
+    assert s0.size() == 7 * 7 * 7 * 7 * 4 * 2 * 6 * 4 * 2
     s14 = sp.Space(sp.OP_CONV, (16, 512, 14, 14, 512, 3, 3, 1, 1))
     assert s14.values[1] == [1, 2, 4, 8, 16] == s14.values[2]
     s32 = sp.Space(sp.OP_CONV, (1, 8, 32, 32, 16, 3, 3, 1, 1))
     assert s32.values[1] == [1, 2, 4, 8, 16, 32] == s32.values[2]   # 32 covers 32
+    assert s32.values[6] == [1, 2, 4, 8]                  # C = 8 clips the splits
     s2 = sp.Space(sp.OP_CONV, (1, 3, 224, 224, 64, 7, 7, 2, 3))
     assert s2.values[1] == [1, 2, 4, 8, 16, 32, 64]       # P = 112: nothing covers it
     assert s2.values[3] == [1, 2] and s2.values[6] == [1, 2]
