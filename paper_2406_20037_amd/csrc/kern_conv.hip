@@ -795,7 +795,7 @@ __device__ __forceinline__ void copy(const char *base, unsigned off, float *dst)
 }  // namespace q4
 
 // Waves per SIMD each conv_mfma2 instance is compiled to allow: the most of
-// 4 and 3 for which its registers fit without spilling (found by compiling
+// 4, 3 and 2 for which its registers fit without spilling (found by compiling
 // every instance under each bound); others keep the compiler's choice.  On
 // its own the compiler keeps the accumulators in AGPRs beside the VGPRs and
 // ends at fewer waves: conv_mfma2<4, 4, 1, 1>, for one, takes 164 VGPRs + 64
@@ -811,12 +811,15 @@ constexpr int kConv2Waves4[] = {
 constexpr int kConv2Waves3[] = {
     10821, 10822, 10841, 10842, 20421, 20422, 20441, 20442, 20811, 20812, 40241, 40242,
     40411, 40412};
+constexpr int kConv2Waves2[] = {11621, 20821, 20841, 40441, 40811};
 constexpr int conv2_waves(int tkb, int npb, int u, int kg) {
     const int key = tkb * 10000 + npb * 100 + u * 10 + kg;
     for (int k : kConv2Waves4)
         if (k == key) return 4;
     for (int k : kConv2Waves3)
         if (k == key) return 3;
+    for (int k : kConv2Waves2)
+        if (k == key) return 2;
     return 1;
 }
 
