@@ -87,6 +87,23 @@ def counters(db):
     return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
 
 
+def paired_reduce(cur, kname, threads, red):
+    """Durations of the reduce dispatches that directly follow (in start time)
+    a dispatch of kname at the given grid: the reduce launch of that split
+    schedule, not the same reduce kernel of other tasks.  Empty when the
+    trace has no start times."""
+    cols = [c[0] for c in cur.execute("select * from kernels limit 1").description]
+    if "start" not in cols:
+        return []
+    seq = list(cur.execute('select name, start, duration, grid_x * grid_y * grid_z from kernels '
+                           'order by start'))
+    out = []
+    for (name, _, _, g), nxt in zip(seq, seq[1:]):
+        if short(name) == kname and (threads is None or g == threads) and short(nxt[0]) == red:
+            out.append(nxt[2])
+    return sorted(out)
+
+
 def bench_check(db, bench_json):
     """The dominant kernel of a profiled bench.py run: its traced dispatches at
     the tuned launch shape against the average launch time bench.py reported
@@ -116,13 +133,15 @@ def bench_check(db, bench_json):
     print(f"| `{kname}` | {len(at)} of {len(durs)} | {mean:.3f} | {med:.3f} | {at[0] / 1e3:.3f} |")
     total = med
     if red:
-        # (every split schedule of this split count and output-size class
-        # launches the same reduce grid; its median is the common case)
-        rd = sorted(d for name, d, g in rows if short(name) == red and (rgrid is None or g == rgrid))
+        rd, how = paired_reduce(cur, kname, threads, red), "after each of them"
+        if not rd:
+            # no dispatch times in the trace: every reduce of that grid
+            rd = sorted(d for name, d, g in rows if short(name) == red and (rgrid is None or g == rgrid))
+            how = "every dispatch of that grid"
         if rd:
             rmed = rd[len(rd) // 2] / 1e3
             total += rmed
-            print(f"| `{red}` | {len(rd)} | {sum(rd) / len(rd) / 1e3:.3f} | {rmed:.3f} | "
+            print(f"| `{red}` ({how}) | {len(rd)} | {sum(rd) / len(rd) / 1e3:.3f} | {rmed:.3f} | "
                   f"{rd[0] / 1e3:.3f} |")
     print(f"\nTraced median per layer launch {total:.3f} us against the bench's "
           f"{rf['avg_launch_us']:.3f} us (difference {rf['avg_launch_us'] - total:.3f} us, "

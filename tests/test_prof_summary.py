@@ -1,0 +1,47 @@
+"""Host logic of the profile summaries (no GPU): kernel-name shortening and the
+pairing of a split schedule's conv dispatches with the reduce launch that
+follows each of them in a kernel trace."""
+import sqlite3
+
+from paper_2406_20037_amd import prof_summary as ps
+
+CONV = "void ds::(anonymous namespace)::conv_mfma2<2, 8, 2, 1>(ds::Conv2Args)"
+RED = "void ds::(anonymous namespace)::split_reduce_kernel<8>(float const*, float*, long)"
+OTHER = "void ds::(anonymous namespace)::conv_mfma2<4, 4, 1, 1>(ds::Conv2Args)"
+
+
+def trace(rows, with_start=True):
+    cur = sqlite3.connect(":memory:").cursor()
+    if with_start:
+        cur.execute("create table kernels(name text, start int, duration int, grid_x int, "
+                    "grid_y int, grid_z int)")
+        cur.executemany("insert into kernels values (?,?,?,?,?,?)",
+                        [(n, s, d, g, 1, 1) for n, s, d, g in rows])
+    else:
+        cur.execute("create table kernels(name text, duration int, grid_x int, grid_y int, "
+                    "grid_z int)")
+        cur.executemany("insert into kernels values (?,?,?,?,?)",
+                        [(n, d, g, 1, 1) for n, _, d, g in rows])
+    return cur
+
+
+def test_short_names():
+    assert ps.short(CONV) == "conv_mfma2<2, 8, 2, 1>"
+    assert ps.short(RED) == "split_reduce_kernel<8>"
+
+
+def test_reduce_paired_with_the_dispatch_before_it():
+    rows = [(CONV, 0, 590, 819200), (RED, 600, 40, 1048576),
+            (OTHER, 650, 500, 802816), (RED, 1200, 100, 1048576),   # another task's reduce
+            (CONV, 2000, 595, 819200), (RED, 2600, 45, 1048576),
+            (CONV, 3000, 597, 409600), (RED, 3600, 70, 1048576)]    # other grid
+    cur = trace(rows)
+    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == [40, 45]
+    # rows inserted out of time order pair the same way
+    cur = trace(list(reversed(rows)))
+    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == [40, 45]
+
+
+def test_no_start_times_gives_no_pairs():
+    cur = trace([(CONV, 0, 590, 819200), (RED, 600, 40, 1048576)], with_start=False)
+    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == []
