@@ -368,15 +368,15 @@ typedef struct {
 } ds_trace;
 
 /*
- * ansor_sample -- a2: draw n_explore points (as ansor_draw) and measure each
- * on the GPU; *best is the fastest (ties: first drawn).  If io->ref is NULL
+ * ansor_sample -- the exploration of the combined approach (Sections 2.1 and
+ * 2.3): draw n_explore points (as ansor_draw) and measure each on the GPU; *best is the fastest (ties: first drawn).  If io->ref is NULL
  * the library computes a reference with kernel_run_reference.
  */
 int ansor_sample(const ds_space *space, uint64_t seed, int n_explore, const ds_tune_io *io,
                  const ds_measure_cfg *cfg, ds_sched *best, double *best_ms, ds_trace *trace);
 
 /*
- * droplet_tune_ex -- a6: Droplet Search (Section 2.2) from start (NULL = the
+ * droplet_tune_ex -- Droplet Search (Section 2.2) from start (NULL = the
  * no-optimisation origin): measure the uncached valid neighbours of the
  * current point, move to the fastest if it is faster (median lower and, for
  * alpha < 1, one-sided rank-sum p < alpha, the 95% criterion of Section 3
@@ -389,7 +389,7 @@ int droplet_tune_ex(const ds_space *space, const ds_sched *start, int budget,
                     ds_tune_result *res, ds_trace *trace);
 
 /*
- * ds_tune -- a7, the combined approach (Section 2.3): explore cfg->n_explore
+ * ds_tune -- the combined approach (Section 2.3): explore cfg->n_explore
  * samples, give the best to Droplet Search with cfg->budget, run it to
  * convergence.  Samples are cached, so Droplet never re-measures them.
  */
@@ -418,9 +418,10 @@ int ds_cache_size(const ds_cache *cache);
 int ds_cache_get(const ds_cache *cache, const ds_sched *s, ds_measurement *out);
 
 /*
- * ds_explore -- a2 alone: draw cfg->n_explore points (as ansor_draw with
- * cfg->seed) and measure each into cache; a point already cached keeps its
- * measurement and is not measured again.  res->seed_point / seed_ms (and
+ * ds_explore -- the exploration alone (Section 2.3, first step): draw
+ * cfg->n_explore points (as ansor_draw with cfg->seed) and measure each into
+ * cache; a point already cached keeps its measurement and is not measured
+ * again.  res->seed_point / seed_ms (and
  * best / best_ms) are the fastest drawn point (ties: first drawn);
  * n_explore_measured counts new measurements; n_failed and explore_s are
  * filled.  DS_EEXHAUSTED if nothing can be drawn.
