@@ -278,6 +278,13 @@ def main(argv=None):
     for n in names:
         W[n].tune(L, wl, args, stream, final_cfg)
     floor = L.ds_empty_kernel_floor(stream)
+    # The fp32 MFMA rate this device sustains with no memory traffic (the
+    # library's calibration launch), beside the published peak.
+    sink = torch.empty(L.DS_MFMA_CEILING_SINK, device="cuda:0")
+    ceil_m, ceil_flop = L.ds_mfma_ceiling(sink, iters=512, stream=stream,
+                                          cfg=L.measure_cfg(repeat=7))
+    ceiling_tflops = ceil_flop / (ceil_m.median_ms * 1e-3) / 1e12
+    del sink
 
     # Timed region: passes of the headline network, then of the other workloads.
     torch.cuda.synchronize()
@@ -351,6 +358,9 @@ def main(argv=None):
                     "achieved": round(ach / 1e12, 3), "peak": PEAK_FP32_TFLOPS,
                     "unit": "TFLOP/s"}
     roofline["frac"] = round(roofline["achieved"] / roofline["peak"], 4)
+    if roofline["unit"] == "TFLOP/s":
+        roofline["mfma_ceiling"] = round(ceiling_tflops, 2)
+        roofline["frac_of_ceiling"] = round(roofline["achieved"] / ceiling_tflops, 4)
     # A split schedule is two launches per layer (the kernel, then the reduce
     # of its partial outputs): the events time both, and so does the traffic.
     splits = task["space"].kernel_info(task["best"].index())["splits"]
@@ -396,6 +406,7 @@ def main(argv=None):
                                     for c in configs),
             "tuning_wall_s_total": round(sum(c["tuning_wall_s"] for c in configs), 2),
             "empty_kernel_floor_us": round(floor.median_ms * 1e3, 3),
+            "mfma_ceiling_tflops": round(ceiling_tflops, 2),
             "device": info,
         },
         "parity": None if worst is None else {

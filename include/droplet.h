@@ -323,6 +323,24 @@ int ds_measure(const ds_sched *s, const ds_tune_io *io, const ds_measure_cfg *cf
  * host launches or graph replays as cfg->graph says. */
 int ds_empty_kernel_floor(hipStream_t stream, const ds_measure_cfg *cfg, ds_measurement *out);
 
+/* Floats the sink of ds_mfma_ceiling must hold: one per thread of its grid
+ * (1024 workgroups of 256 threads). */
+#define DS_MFMA_CEILING_SINK 262144
+
+/* ds_mfma_ceiling -- the fp32 MFMA rate this device sustains with no memory
+ * traffic: every wave (four on each SIMD) issues back-to-back 16x16x4 fp32
+ * MFMAs into 16 independent accumulator blocks, iters rounds of 16.  A
+ * calibration of the measurement, like the empty-kernel floor (the paper
+ * defines no such operation): the rate the tuned MFMA kernels can approach on
+ * this device, next to the published peak, which assumes the nominal clock.
+ * sink: device buffer of at least
+ * DS_MFMA_CEILING_SINK floats, owned by the caller, overwritten.  Launches
+ * one timed kernel per repeat (cfg->warmup untimed first); *flop receives
+ * the flop of one launch, out->median_ms its time.  Errors: DS_EINVAL (null
+ * pointer, iters < 1, sink too small), DS_EHIP. */
+int ds_mfma_ceiling(hipStream_t stream, float *sink, int64_t sink_elems, int iters,
+                    const ds_measure_cfg *cfg, ds_measurement *out, double *flop);
+
 /* ---- tuning --------------------------------------------------------------- */
 
 /* A measurement callback: fills *out for schedule s, returns DS_OK or an error

@@ -172,6 +172,9 @@ SIGNATURES = {
                              C.c_double, C.POINTER(ds_measurement)]),
     "ds_empty_kernel_floor": (C.c_int, [C.c_void_p, C.POINTER(ds_measure_cfg),
                                         C.POINTER(ds_measurement)]),
+    "ds_mfma_ceiling": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_int,
+                                  C.POINTER(ds_measure_cfg), C.POINTER(ds_measurement),
+                                  C.POINTER(C.c_double)]),
     "ds_tune_cfg_default": (None, [C.POINTER(ds_tune_cfg)]),
     "ansor_sample": (C.c_int, [C.c_void_p, C.c_uint64, C.c_int, C.POINTER(ds_tune_io),
                                C.POINTER(ds_measure_cfg), C.POINTER(ds_sched),
@@ -429,6 +432,20 @@ def ds_empty_kernel_floor(stream=None, cfg=None):
           lib.ds_empty_kernel_floor(stream_handle(stream), C.byref(cfg) if cfg else None,
                                     C.byref(m)))
     return m
+
+
+DS_MFMA_CEILING_SINK = 262144
+
+
+def ds_mfma_ceiling(sink, iters=512, stream=None, cfg=None):
+    """(measurement, flop per launch) of the library's pure-MFMA calibration
+    kernel; sink is a float32 device tensor of >= DS_MFMA_CEILING_SINK elements."""
+    m = ds_measurement()
+    flop = C.c_double()
+    check("ds_mfma_ceiling",
+          lib.ds_mfma_ceiling(stream_handle(stream), ptr(sink), sink.numel(), iters,
+                              C.byref(cfg) if cfg else None, C.byref(m), C.byref(flop)))
+    return m, flop.value
 
 
 def _trace(cap):

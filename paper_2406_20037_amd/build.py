@@ -26,7 +26,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["space.cpp", "tuner.cpp"]
-HIP_SOURCES = ["harness.hip"]
+HIP_SOURCES = ["harness.hip", "kern_reduce.hip"]
 SLICED_SOURCES = ["kern_conv.hip", "kern_matmul.hip"]
 
 HIP_FLAGS = [

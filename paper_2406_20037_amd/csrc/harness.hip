@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "kern_common.h"
+#include "kern_reduce.h"
 
 namespace ds {
 
@@ -57,49 +58,7 @@ __global__ void fill_kernel(float *p, int64_t n, float v) {
     if (tid < n - t0) p[t0 + tid] = v;
 }
 
-// y[i] = sum over z < S of part[z * n + i], summed in split order.  S is a
-// template parameter so every thread issues its S loads before the first add.
-template <int S>
-__global__ __launch_bounds__(256) void split_reduce_kernel(const float *__restrict__ part,
-                                                           float *__restrict__ y, int64_t n) {
-    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-    const bool vec = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(y) % 16 == 0) &&
-                     (reinterpret_cast<uintptr_t>(part) % 16 == 0);
-    if (vec) {
-        const int64_t n4 = n / 4;
-        const floatx4 *p4 = reinterpret_cast<const floatx4 *>(part);
-        for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n4; i += stride) {
-            floatx4 v[S];
-#pragma unroll
-            for (int z = 0; z < S; ++z) v[z] = p4[z * n4 + i];
-            floatx4 s = v[0];
-#pragma unroll
-            for (int z = 1; z < S; ++z) s += v[z];
-            reinterpret_cast<floatx4 *>(y)[i] = s;
-        }
-    } else {
-        for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-            float v[S];
-#pragma unroll
-            for (int z = 0; z < S; ++z) v[z] = part[z * n + i];
-            float s = v[0];
-#pragma unroll
-            for (int z = 1; z < S; ++z) s += v[z];
-            y[i] = s;
-        }
-    }
-}
-
-constexpr int kMaxSplits = 32;
-
-template <int... S>
-constexpr std::array<const void *, sizeof...(S) + 2> split_reduce_table(
-    std::integer_sequence<int, S...>) {
-    return {nullptr, nullptr, reinterpret_cast<const void *>(&split_reduce_kernel<S + 2>)...};
-}
-// kSplitReduce[S]: the reduce kernel of S partial slices, 2 <= S <= kMaxSplits
-const std::array<const void *, kMaxSplits + 1> kSplitReduce =
-    split_reduce_table(std::make_integer_sequence<int, kMaxSplits - 1>{});
+constexpr int kCeilBlocks = 16;                // accumulator blocks per wave
 
 __global__ void fill_u32_kernel(unsigned *p, int n) {
     if (int(threadIdx.x) < n) p[threadIdx.x] = 0u;
@@ -131,6 +90,27 @@ __global__ __launch_bounds__(256) void parity_kernel(const float *y, const float
 }
 
 __global__ void empty_kernel() {}
+
+// The fp32 MFMA pipe under a pure MFMA load: every wave issues back-to-back
+// 16x16x4 MFMAs into 16 independent accumulator blocks from register
+// operands, with no memory access in the loop; one float per thread leaves
+// through sink so the work is kept.
+__global__ __launch_bounds__(256) void mfma_ceiling_kernel(float *sink, int iters) {
+    const int lane = threadIdx.x & 63;
+    const float a = 1.0f + 1e-3f * lane, b = 1.0f - 1e-3f * lane;
+    floatx4 acc[kCeilBlocks];
+#pragma unroll
+    for (int i = 0; i < kCeilBlocks; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int i = 0; i < kCeilBlocks; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[i], 0, 0, 0);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kCeilBlocks; ++i) s += acc[i][0] + acc[i][1] + acc[i][2] + acc[i][3];
+    sink[int64_t(blockIdx.x) * blockDim.x + threadIdx.x] = s;
+}
 
 // One thread per output, reduction in the definition's order (c, r, s / k).
 __global__ __launch_bounds__(256) void conv_ref_kernel(ConvArgs a) {
@@ -681,8 +661,8 @@ int launch_plan(const Plan &plan, hipStream_t stream) {
         const int64_t blocks = std::min<int64_t>(cdiv64(n4, 256), 4096);
         int64_t n = plan.y_elems;
         void *rargs[] = {const_cast<float **>(&part), &y, &n};
-        if (!hip_ok(hipLaunchKernel(kSplitReduce[plan.splits], dim3(unsigned(blocks)), dim3(256),
-                                    rargs, 0, stream),
+        if (!hip_ok(hipLaunchKernel(split_reduce_kernel_for(plan.splits), dim3(unsigned(blocks)),
+                                    dim3(256), rargs, 0, stream),
                     "split reduce launch"))
             return DS_EHIP;
         if (!hip_ok(hipGetLastError(), "split reduce launch")) return DS_EHIP;
@@ -953,6 +933,40 @@ int ds_empty_kernel_floor(hipStream_t stream, const ds_measure_cfg *cfg_in, ds_m
     else rc = time_repeats(launch, stream, number, cfg.repeat, out->repeats_ms);
     if (rc != DS_OK) return rc;
     out->number = number;
+    summarise(out, cfg.repeat);
+    return DS_OK;
+}
+
+int ds_mfma_ceiling(hipStream_t stream, float *sink, int64_t sink_elems, int iters,
+                    const ds_measure_cfg *cfg_in, ds_measurement *out, double *flop) {
+    if (!sink || !out || !flop || iters < 1) {
+        set_error("bad ds_mfma_ceiling arguments");
+        return DS_EINVAL;
+    }
+    if (sink_elems < DS_MFMA_CEILING_SINK) {
+        set_error("ds_mfma_ceiling needs a sink of %lld floats, got %lld",
+                  (long long)DS_MFMA_CEILING_SINK, (long long)sink_elems);
+        return DS_EINVAL;
+    }
+    std::memset(out, 0, sizeof *out);
+    ds_measure_cfg cfg;
+    if (cfg_in) cfg = *cfg_in;
+    else ds_measure_cfg_default(&cfg);
+    cfg.repeat = std::max(1, std::min(cfg.repeat, DS_MAX_REPEATS));
+    // four waves on each of the 1024 SIMDs of a 256-CU part
+    const int blocks = int(DS_MFMA_CEILING_SINK / 256);
+    *flop = double(blocks) * 4 * iters * kCeilBlocks * 2048.0;
+    auto launch_on = [&](hipStream_t st) {
+        hipLaunchKernelGGL(mfma_ceiling_kernel, dim3(blocks), dim3(256), 0, st, sink, iters);
+        return hip_ok(hipGetLastError(), "mfma ceiling launch") ? DS_OK : DS_EHIP;
+    };
+    auto launch = [&]() { return launch_on(stream); };
+    double w[1];
+    int rc = time_repeats(launch, stream, std::max(1, cfg.warmup), 1, w);
+    if (rc != DS_OK) return rc;
+    rc = time_repeats(launch, stream, 1, cfg.repeat, out->repeats_ms);
+    if (rc != DS_OK) return rc;
+    out->number = 1;
     summarise(out, cfg.repeat);
     return DS_OK;
 }

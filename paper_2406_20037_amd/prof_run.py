@@ -23,7 +23,10 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="matmul_1024",
                     help="a single-kernel workload or a network layer (resnet50:NAME, vgg16:NAME)")
-    ap.add_argument("--sched", required=True, help="knob=value,... (every axis)")
+    ap.add_argument("--sched", help="knob=value,... (every axis)")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="launch the library's pure-MFMA calibration kernel --iters times "
+                         "instead of a schedule")
     ap.add_argument("--iters", type=int, default=100)
     ap.add_argument("--copy-mib", type=int, default=64)
     ap.add_argument("--host-launch", action="store_true",
@@ -36,6 +39,16 @@ def main(argv=None):
     from synthdata import workloads as wl
     from paper_2406_20037_amd import _lib as L
 
+    if args.mfma_ceiling:
+        sink = torch.empty(L.DS_MFMA_CEILING_SINK, device="cuda:0")
+        m, flop = L.ds_mfma_ceiling(sink, iters=512,
+                                    cfg=L.measure_cfg(warmup=1, repeat=args.iters))
+        torch.cuda.synchronize()
+        print(f"ran {args.iters + 1} x mfma_ceiling_kernel: median {m.median_ms * 1e3:.1f} us, "
+              f"{flop / (m.median_ms * 1e-3) / 1e12:.1f} TFLOP/s", flush=True)
+        return 0
+    if not args.sched:
+        ap.error("--sched is required unless --mfma-ceiling")
     if ":" in args.workload:          # a network layer, e.g. vgg16:L6_256_256_56
         net, layer = args.workload.split(":", 1)
         table = {"resnet50": wl.RESNET50, "vgg16": wl.VGG16}[net]

@@ -23,7 +23,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = {
     "mm_": ["csrc/kern_matmul.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
     "conv_": ["csrc/kern_conv.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
-    "split_reduce_kernel": ["csrc/harness.hip", "csrc/kern_common.h", "csrc/ds_internal.h"],
+    "split_reduce_kernel": ["csrc/kern_reduce.hip", "csrc/kern_reduce.h", "csrc/kern_common.h"],
 }
 
 

@@ -260,6 +260,28 @@ def test_error_paths_without_gpu():
         lib.droplet_tune_ex(m, None, 10, None, None, None)   # GPU mode needs buffers
 
 
+class _FakeSink:
+    """Stands for a device tensor: an address and an element count (the
+    argument checks run before anything touches the device)."""
+    def __init__(self, n, addr=0x10000):
+        self.n, self.addr = n, addr
+
+    def data_ptr(self):
+        return self.addr
+
+    def numel(self):
+        return self.n
+
+
+def test_mfma_ceiling_argument_errors_without_gpu():
+    with pytest.raises(lib.DsError, match="DS_EINVAL"):
+        lib.ds_mfma_ceiling(_FakeSink(lib.DS_MFMA_CEILING_SINK, addr=0))     # null sink
+    with pytest.raises(lib.DsError, match="DS_EINVAL"):
+        lib.ds_mfma_ceiling(_FakeSink(lib.DS_MFMA_CEILING_SINK - 1))        # sink too small
+    with pytest.raises(lib.DsError, match="DS_EINVAL"):
+        lib.ds_mfma_ceiling(_FakeSink(lib.DS_MFMA_CEILING_SINK), iters=0)
+
+
 def test_single_hip_runtime_in_process():
     """Loading the binding first must not map a second HIP runtime next to torch's."""
     import subprocess

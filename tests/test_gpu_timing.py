@@ -94,3 +94,21 @@ def test_timing_is_physical_and_stable(torch_dev, lib, workload, layer, knobs):
         assert rate <= PEAK_FLOPS, f"{rate / 1e12:.1f} TFLOP/s exceeds the fp32 peak"
     assert abs(a.median_ms - b.median_ms) <= 0.15 * min(a.median_ms, b.median_ms)
     del keep
+
+
+def test_mfma_ceiling_is_physical(torch_dev, lib):
+    """The pure-MFMA calibration launch: a rate under the published fp32 peak
+    and above half of it, its median at its fastest repeats."""
+    torch, L = torch_dev, lib
+    sink = torch.empty(L.DS_MFMA_CEILING_SINK, device="cuda:0")
+    print("mfma ceiling", flush=True)
+    m, flop = L.ds_mfma_ceiling(sink, iters=512, cfg=L.measure_cfg(repeat=7))
+    torch.cuda.synchronize()
+    assert m.status == 0 and m.n_repeats == 7
+    assert flop == 1024 * 4 * 512 * 16 * 2048
+    rate = flop / (m.median_ms * 1e-3)
+    assert 0.5 * PEAK_FLOPS < rate <= PEAK_FLOPS, f"{rate / 1e12:.1f} TFLOP/s"
+    # single host launches: an occasional slow one, but the median sits at
+    # the fast ones
+    assert m.median_ms <= 1.1 * m.min_ms, [m.repeats_ms[i] for i in range(m.n_repeats)]
+    assert bool(torch.isfinite(sink).all())
