@@ -6,7 +6,8 @@ profiling a single kernel instance with rocprofv3.
 
 The schedule is launched the way the tuner times it: --iters launches captured
 in a HIP graph and replayed back to back (--host-launch: one host launch per
-iteration instead).  The copy (torch's elementwise copy of --copy-mib MiB)
+iteration instead; with --flush-mb, each after a write of that many MiB that
+evicts the caches).  The copy (torch's elementwise copy of --copy-mib MiB)
 gives the factor that relates the HBM counters to bytes actually moved.
 """
 from __future__ import annotations
@@ -31,6 +32,9 @@ def main(argv=None):
     ap.add_argument("--copy-mib", type=int, default=64)
     ap.add_argument("--host-launch", action="store_true",
                     help="launch from the host one by one instead of a replayed graph")
+    ap.add_argument("--flush-mb", type=int, default=0,
+                    help="with --host-launch: write this many MiB of scratch before every "
+                         "launch, so each one starts with cold L2 and MALL (their 256 MiB)")
     args = ap.parse_args(argv)
 
     import torch
@@ -69,8 +73,14 @@ def main(argv=None):
         n_out = shape[0] * shape[1]
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     yd = torch.empty(n_out, device="cuda:0")
+    if args.flush_mb and not args.host_launch:
+        ap.error("--flush-mb needs --host-launch")
     if args.host_launch:
+        scratch = (torch.empty(args.flush_mb * (1 << 20) // 4, device="cuda:0")
+                   if args.flush_mb else None)
         for _ in range(args.iters):
+            if scratch is not None:
+                scratch.fill_(1.0)
             L.kernel_run(op, s, xd, wd, yd)
     else:
         # a first and a warm-up launch, then a graph of --iters launches replayed
