@@ -799,7 +799,7 @@ __device__ __forceinline__ void copy(const char *base, unsigned off, float *dst)
 // every instance under each bound); others keep the compiler's choice.  On
 // its own the compiler keeps the accumulators in AGPRs beside the VGPRs and
 // ends at fewer waves: conv_mfma2<4, 4, 1, 1>, for one, takes 164 VGPRs + 64
-// AGPRs (2 waves) unbounded and 152 VGPRs (3 waves) bounded.  An instance is
+// AGPRs (2 waves) unbounded and 119 VGPRs (4 waves) bounded.  An instance is
 // keyed TKB·10000 + NPB·100 + U·10 + KG.
 constexpr int kConv2Waves4[] = {
     10111, 10112, 10114, 10121, 10122, 10124, 10141, 10142, 10144, 10211, 10212, 10214,
@@ -807,11 +807,12 @@ constexpr int kConv2Waves4[] = {
     10441, 10442, 10444, 10811, 10812, 20111, 20112, 20114, 20121, 20122, 20124, 20141,
     20142, 20144, 20211, 20212, 20214, 20221, 20222, 20224, 20241, 20242, 20244, 20411,
     20412, 40111, 40112, 40114, 40121, 40122, 40124, 40141, 40142, 40144, 40211, 40212,
-    40221, 40222};
+    40221, 40222, 40411, 40412};
 constexpr int kConv2Waves3[] = {
-    10821, 10822, 10841, 10842, 20421, 20422, 20441, 20442, 20811, 20812, 40241, 40242,
-    40411, 40412};
-constexpr int kConv2Waves2[] = {11621, 20821, 20841, 40441, 40811};
+    10821, 10822, 10841, 10842, 11611, 20421, 20422, 20441, 20442, 20811, 20812, 40241,
+    40242};
+constexpr int kConv2Waves2[] = {
+    11621, 11641, 20821, 20841, 21611, 40441, 40811};
 constexpr int conv2_waves(int tkb, int npb, int u, int kg) {
     const int key = tkb * 10000 + npb * 100 + u * 10 + kg;
     for (int k : kConv2Waves4)
@@ -894,14 +895,15 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_m
     // (held only when the workgroup walks more than one chunk: a single
     // chunk's units are computed as they are issued, so the first copies leave
     // sooner)
+    constexpr int RC = conv2_reg_copies(TKB, NPB, U, KG);
     const bool reuse = a.regs && ci1 - ci0 > 1;
-    int sw[kConv2RegCopies], sh[kConv2RegCopies];
+    int sw[RC], sh[RC];
     if (reuse) {
         q4::Cursor cur;
         cur.start(a, tid);
         const int gw = a.vw ? 4 : 1, gh = a.vh ? 4 : 1;
 #pragma unroll
-        for (int u = 0; u < kConv2RegCopies; ++u) {
+        for (int u = 0; u < RC; ++u) {
             sw[u] = sh[u] = -1;
             if (u < a.ncopy) {
                 const int kl = min(cur.kl, kvalid - 1);
@@ -921,7 +923,7 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_m
         float *wt = smem + b * a.buf;
         float *xs = wt + a.bufw;
 #pragma unroll
-        for (int u = 0; u < kConv2RegCopies; ++u) {
+        for (int u = 0; u < RC; ++u) {
             if (u >= a.ncopy) break;
             const int d = u * nthr + slot;
             if (sw[u] >= 0) {
@@ -936,8 +938,9 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_m
     };
     // Units computed as they are issued: a chunk with channel slots past C
     // (its buffer zeroed first), a workgroup's only chunk, or every chunk when
-    // a thread's units do not fit its registers (4-byte copies of misaligned
-    // operands).
+    // a thread's units do not fit the registers the instance holds them in
+    // (more than RC units: 4-byte copies of misaligned operands, or a
+    // large-tile instance).
     auto issue_units = [&](int ci, int b, bool zero) {
         float *wt = smem + b * a.buf;
         float *xs = wt + a.bufw;

@@ -164,7 +164,7 @@ bool replay(const int64_t *sh, int tk, int th, int tw, int tc, int depth, int ks
                 if (e + i < src.size() && dst + i >= 0 && dst + i < lds_f) lds[dst + i] = src[e + i];
         };
         const bool reuse = a.regs && ci1 - ci0 > 1;
-        std::vector<int> sw(size_t(nthr) * kConv2RegCopies, -1), shv(size_t(nthr) * kConv2RegCopies, -1);
+        std::vector<int> sw(size_t(nthr) * kConv2MaxCopies, -1), shv(size_t(nthr) * kConv2MaxCopies, -1);
         if (reuse) {
             for (int tid = 0; tid < nthr; ++tid) {
                 Cursor cur;
@@ -173,11 +173,11 @@ bool replay(const int64_t *sh, int tk, int th, int tw, int tc, int depth, int ks
                 for (int u = 0; u < a.ncopy; ++u) {
                     const int kl = std::min(cur.kl, kvalid - 1);
                     const int col = std::min(gw * cur.wc, a.tc * RS - gw);
-                    sw[tid * kConv2RegCopies + u] = cur.kl < a.tk ? 4 * (kl * C * RS + col) : -1;
+                    sw[tid * kConv2MaxCopies + u] = cur.kl < a.tk ? 4 * (kl * C * RS + col) : -1;
                     const int hy = fdv(cur.hu, a.f_hru);
                     const int hx = gh * (cur.hu - hy * a.hr_u);
                     const int o = halo_src(cur.hc, hy, hx);
-                    shv[tid * kConv2RegCopies + u] = cur.hc >= tc4 ? -1 : hy >= a.hs ? 0 : o >= 0 ? 4 * o : -1;
+                    shv[tid * kConv2MaxCopies + u] = cur.hc >= tc4 ? -1 : hy >= a.hs ? 0 : o >= 0 ? 4 * o : -1;
                     cur.next(a);
                 }
             }
@@ -193,7 +193,7 @@ bool replay(const int64_t *sh, int tk, int th, int tw, int tc, int depth, int ks
                 if (creal >= tc4 && reuse) {
                     for (int u = 0; u < a.ncopy; ++u) {
                         const int d = u * nthr + lane_base + lane;
-                        const int ow = sw[tid * kConv2RegCopies + u], oh = shv[tid * kConv2RegCopies + u];
+                        const int ow = sw[tid * kConv2MaxCopies + u], oh = shv[tid * kConv2MaxCopies + u];
                         if (ow >= 0) copy(w, wb, ow, a.vw ? 4 : 1, a.vw ? wt + 4 * d : wt + d);
                         if (oh >= 0) copy(x, xb, oh, a.vh ? 4 : 1, a.vh ? xs + 4 * d : xs + d);
                     }
