@@ -159,7 +159,7 @@ struct Conv2Args {
     int vw, vh;           // 16-byte copies of weight / halo units (else 4-byte)
     int nw4, nh4;         // copy units of a chunk (weights, halo)
     int ncopy;            // copy units per thread per kind
-    int rc;               // copy units per thread the instance holds in registers
+    int rc;               // copy units per thread the instance holds in registers (RC)
     int regs;             // ncopy <= rc: a full chunk's sources stay in registers
     int wr_u, hc_u, hr_u; // copy units per weight row, halo channel, halo row
     int w_dk, w_dc;       // blockDim in (weight row, unit) mixed radix
@@ -180,15 +180,11 @@ struct Conv2Shape {
 
 constexpr int kConv2MaxCopies = 12;       // copy units per thread of a valid point
 
-// Copy units per thread an instance keeps in registers across chunks: 12, or
-// 4 for the instances that run one more wave per SIMD with the registers
-// that frees (conv_mfma2<4,4,1,1> and <4,4,1,2>: 3 -> 4 waves; <1,16,1,1>:
-// 2 -> 3; <1,16,4,1>, <2,16,1,1>: 1 -> 2).  A point with more units than its
-// instance holds recomputes its copy sources at every chunk.
-constexpr int conv2_reg_copies(int tkb, int npb, int u, int kg) {
-    const int key = tkb * 10000 + npb * 100 + u * 10 + kg;
-    return key == 40411 || key == 40412 || key == 11611 || key == 11641 || key == 21611 ? 4 : 12;
-}
+// Copy units per thread a conv_mfma2 instance keeps in registers across
+// chunks (its RC template parameter): 4 when a point needs no more, or when
+// its workgroups walk a single chunk (the registers that frees buy many
+// instances more waves per SIMD), else 12.
+constexpr int kConv2FewCopies = 4;
 
 // Register budget of the compiled conv_mfma2 instances (no spill; launch bound
 // 256 * KG): TKB x NPB blocks per wave and TKB + NPB operand floats per quad.
@@ -203,6 +199,9 @@ inline void conv2_units(Conv2Args &a, int threads) {
     a.nw4 = a.vw ? a.bufw / 4 : a.bufw;
     a.nh4 = int(a.vh ? int64_t(tc4) * a.cs / 4 : std::min<int64_t>(int64_t(tc4) * a.cs, INT32_MAX));
     a.ncopy = std::max((a.nw4 + threads - 1) / threads, (a.nh4 + threads - 1) / threads);
+    // (a workgroup that walks one chunk never reuses its sources: the 4-unit
+    // instance, whatever the count)
+    a.rc = a.ncopy <= kConv2FewCopies || a.cps <= 1 ? kConv2FewCopies : kConv2MaxCopies;
     a.regs = a.ncopy <= a.rc;
     a.wr_u = a.vw ? a.wrow / 4 : a.wrow;
     a.hc_u = a.vh ? a.cs / 4 : a.cs;
@@ -300,7 +299,6 @@ inline Conv2Shape conv2_setup(const int64_t *sh, int tk, int th, int tw, int tc,
     a.buf = int(std::min<int64_t>(buf, INT32_MAX));
     a.nbuf = a.cps > 1 ? 2 : 1;
     g.threads = 64 * a.wpx * kg;
-    a.rc = conv2_reg_copies(g.tkb, g.npb, g.u, kg);
     conv2_units(a, g.threads);
     // a full chunk's copy units are held in registers (chunks with channel
     // slots past C, C < 4, compute theirs as they go)
@@ -389,7 +387,7 @@ int launch_plan(const Plan &plan, hipStream_t stream);
 // Kernel instance lookup (compiled template instances).
 const void *conv_valu_instance(int kpt, int ppt, int uf, int lds);
 const void *conv_mfma_instance(int tkb, int npb, int d, int lds);
-const void *conv_mfma2_instance(int tkb, int npb, int u, int kg);
+const void *conv_mfma2_instance(int tkb, int npb, int u, int kg, int rc);
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf);
 const void *mm_mfma_instance(int wm, int wn, int bk, int uf, int dbuf, int kg);
 int count_instances();

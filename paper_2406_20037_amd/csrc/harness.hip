@@ -421,10 +421,11 @@ const void *conv_mfma_instance(int tkb, int npb, int d, int lds) {
     return g_conv_mfma[((a * 7 + b) * 3 + d - 1) * 2 + lds];
 }
 
-const void *conv_mfma2_instance(int tkb, int npb, int u, int kg) {
+const void *conv_mfma2_instance(int tkb, int npb, int u, int kg, int rc) {
     const int a = log2_exact(tkb), b = log2_exact(npb), c = log2_exact(u), d = log2_exact(kg);
     if (a < 0 || a > 2 || b < 0 || b > 5 || c < 0 || c > 2 || d < 0 || d > 2) return nullptr;
-    return g_conv_mfma2[((a * 6 + b) * 3 + c) * 3 + d];
+    if (rc != kConv2FewCopies && rc != kConv2MaxCopies) return nullptr;
+    return g_conv_mfma2[(((a * 6 + b) * 3 + c) * 3 + d) * 2 + (rc == kConv2FewCopies)];
 }
 
 const void *mm_valu_instance(int rm, int rn, int bk, int uf, int dbuf) {
@@ -496,13 +497,13 @@ int make_plan(const ds_sched *s, const float *x, const float *w, float *y, Plan 
         // 16-byte output stores only into a 16-byte aligned output (and
         // partials: the workspace is)
         if (reinterpret_cast<uintptr_t>(y) % 16 != 0) a.st4 = 0;
-        plan.func = conv_mfma2_instance(c.tkb, c.npb, c.u, c.kg);
+        plan.func = conv_mfma2_instance(c.tkb, c.npb, c.u, c.kg, a.rc);
         plan.family = DS_KERNEL_CONV_MFMA2;
-        plan.nparams = 4;
-        const int pr[4] = {c.tkb, c.npb, c.u, c.kg};
+        plan.nparams = 5;
+        const int pr[5] = {c.tkb, c.npb, c.u, c.kg, a.rc};
         std::memcpy(plan.params, pr, sizeof pr);
-        plan.slot = ((log2_exact(c.tkb) * 6 + log2_exact(c.npb)) * 3 + log2_exact(c.u)) * 3 +
-                    log2_exact(c.kg);
+        plan.slot = (((log2_exact(c.tkb) * 6 + log2_exact(c.npb)) * 3 + log2_exact(c.u)) * 3 +
+                     log2_exact(c.kg)) * 2 + (a.rc == kConv2FewCopies);
         plan.splits = a.ksw > 1 ? int(cdiv64(a.chunks, a.cps)) : 1;
         plan.y_elems = int64_t(a.N) * a.K * a.P * a.Q;
     } else if (s->op == DS_OP_CONV2D_NCHW) {

@@ -29,7 +29,7 @@ __device__ __forceinline__ void store_out(float *p, float v) { __builtin_nontemp
 // Instance table sizes (one slot per template-parameter tuple).
 constexpr int kConvValuSlots = 7 * 5 * 5 * 2;   // KPT, PPT, UF, LDS
 constexpr int kConvMfmaSlots = 3 * 7 * 3 * 2;   // TKB, NPB, D, LDS
-constexpr int kConvMfma2Slots = 3 * 6 * 3 * 3;  // TKB, NPB, U, KG
+constexpr int kConvMfma2Slots = 3 * 6 * 3 * 3 * 2;  // TKB, NPB, U, KG, RC
 constexpr int kMmValuSlots = 5 * 5 * 5 * 7 * 2; // RM, RN, BK, UF, DB
 constexpr int kMmMfmaSlots = 4 * 4 * 5 * 7 * 2 * 2; // WM, WN, BK, UF, DB, KG
 

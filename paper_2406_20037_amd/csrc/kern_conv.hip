@@ -795,26 +795,56 @@ __device__ __forceinline__ void copy(const char *base, unsigned off, float *dst)
 }  // namespace q4
 
 // Waves per SIMD each conv_mfma2 instance is compiled to allow: the most of
-// 4, 3 and 2 for which its registers fit without spilling (found by compiling
-// every instance under each bound); others keep the compiler's choice.  On
-// its own the compiler keeps the accumulators in AGPRs beside the VGPRs and
-// ends at fewer waves: conv_mfma2<4, 4, 1, 1>, for one, takes 164 VGPRs + 64
-// AGPRs (2 waves) unbounded and 119 VGPRs (4 waves) bounded.  An instance is
-// keyed TKB·10000 + NPB·100 + U·10 + KG.
+// 6, 5, 4, 3 and 2 for which its registers fit without spilling (found by
+// compiling every instance under each bound), separately for the instances
+// that hold 12 copy units per thread in registers and those that hold 4;
+// others keep the compiler's choice.  On its own the compiler keeps the
+// accumulators in AGPRs beside the VGPRs and ends at fewer waves:
+// conv_mfma2<4, 4, 1, 1, 12>, for one, takes 164 VGPRs + 64 AGPRs (2 waves)
+// unbounded and 152 VGPRs (3 waves) bounded; with 4 copy units, 119 VGPRs (4
+// waves).  An instance is keyed TKB·10000 + NPB·100 + U·10 + KG.
 constexpr int kConv2Waves4[] = {
     10111, 10112, 10114, 10121, 10122, 10124, 10141, 10142, 10144, 10211, 10212, 10214,
     10221, 10222, 10224, 10241, 10242, 10244, 10411, 10412, 10414, 10421, 10422, 10424,
     10441, 10442, 10444, 10811, 10812, 20111, 20112, 20114, 20121, 20122, 20124, 20141,
     20142, 20144, 20211, 20212, 20214, 20221, 20222, 20224, 20241, 20242, 20244, 20411,
     20412, 40111, 40112, 40114, 40121, 40122, 40124, 40141, 40142, 40144, 40211, 40212,
-    40221, 40222, 40411, 40412};
+    40221, 40222};
 constexpr int kConv2Waves3[] = {
+    10821, 10822, 10841, 10842, 20421, 20422, 20441, 20442, 20811, 20812, 40241, 40242,
+    40411, 40412};
+constexpr int kConv2Waves2[] = {
+    11621, 20821, 20841, 40441, 40811};
+constexpr int kConv2FewWaves6[] = {
+    10111, 10112, 10114, 10121, 10122, 10124, 10141, 10142, 10144, 10211, 10212, 10214,
+    10221, 10222, 10224, 10241, 10242, 10244, 10411, 10412, 10414, 10421, 10422, 10424,
+    20111, 20112, 20114, 20121, 20122, 20124, 20141, 20142, 20144, 20211, 20212, 20214,
+    20221, 20222, 20224, 20241, 20242, 20244, 40111, 40112, 40114, 40121, 40122, 40124,
+    40141, 40142, 40144, 40211, 40212};
+constexpr int kConv2FewWaves5[] = {
+    10441, 10442, 10444, 10811, 10812, 20411, 20412};
+constexpr int kConv2FewWaves4[] = {
+    40221, 40222, 40411, 40412};
+constexpr int kConv2FewWaves3[] = {
     10821, 10822, 10841, 10842, 11611, 20421, 20422, 20441, 20442, 20811, 20812, 40241,
     40242};
-constexpr int kConv2Waves2[] = {
-    11621, 11641, 20821, 20841, 21611, 40441, 40811};
-constexpr int conv2_waves(int tkb, int npb, int u, int kg) {
+constexpr int kConv2FewWaves2[] = {
+    11621, 11641, 20821, 20822, 20841, 20842, 21611, 40421, 40422, 40441, 40442, 40811};
+constexpr int conv2_waves(int tkb, int npb, int u, int kg, int rc) {
     const int key = tkb * 10000 + npb * 100 + u * 10 + kg;
+    if (rc == kConv2FewCopies) {
+        for (int k : kConv2FewWaves6)
+            if (k == key) return 6;
+        for (int k : kConv2FewWaves5)
+            if (k == key) return 5;
+        for (int k : kConv2FewWaves4)
+            if (k == key) return 4;
+        for (int k : kConv2FewWaves3)
+            if (k == key) return 3;
+        for (int k : kConv2FewWaves2)
+            if (k == key) return 2;
+        return 1;
+    }
     for (int k : kConv2Waves4)
         if (k == key) return 4;
     for (int k : kConv2Waves3)
@@ -824,8 +854,8 @@ constexpr int conv2_waves(int tkb, int npb, int u, int kg) {
     return 1;
 }
 
-template <int TKB, int NPB, int U, int KG>
-__global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_mfma2(Conv2Args a) {
+template <int TKB, int NPB, int U, int KG, int RC>
+__global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG, RC)) void conv_mfma2(Conv2Args a) {
     extern __shared__ float smem[];
     using q4::fdv;
     // tile of this workgroup (tile order: k, q, p, split, image)
@@ -895,7 +925,6 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_m
     // (held only when the workgroup walks more than one chunk: a single
     // chunk's units are computed as they are issued, so the first copies leave
     // sooner)
-    constexpr int RC = conv2_reg_copies(TKB, NPB, U, KG);
     const bool reuse = a.regs && ci1 - ci0 > 1;
     int sw[RC], sh[RC];
     if (reuse) {
@@ -939,8 +968,7 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_m
     // Units computed as they are issued: a chunk with channel slots past C
     // (its buffer zeroed first), a workgroup's only chunk, or every chunk when
     // a thread's units do not fit the registers the instance holds them in
-    // (more than RC units: 4-byte copies of misaligned operands, or a
-    // large-tile instance).
+    // (more than RC units: 4-byte copies of misaligned operands).
     auto issue_units = [&](int ci, int b, bool zero) {
         float *wt = smem + b * a.buf;
         float *xs = wt + a.bufw;
@@ -1171,7 +1199,7 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG)) void conv_m
 // ---- instance registry --------------------------------------------------------
 // conv_valu slots: ((log2 KPT * 5 + log2 PPT) * 5 + log2 UF) * 2 + LDS
 // conv_mfma slots: ((log2 TKB * 7 + log2 NPB) * 3 + D - 1) * 2 + LDS
-// conv_mfma2 slots: ((log2 TKB * 6 + log2 NPB) * 3 + log2 U) * 3 + log2 KG
+// conv_mfma2 slots: (((log2 TKB * 6 + log2 NPB) * 3 + log2 U) * 3 + log2 KG) * 2 + (RC == 4)
 constexpr int kValuSlots = kConvValuSlots;
 constexpr int kMfmaSlots = kConvMfmaSlots;
 
@@ -1207,10 +1235,12 @@ void reg_mfma() {
 
 template <int I>
 void reg_mfma2() {
-    constexpr int ikg = I % 3, iu = (I / 3) % 3, inpb = (I / 9) % 6, itkb = I / 54;
+    constexpr int few = I % 2, J = I / 2;
+    constexpr int ikg = J % 3, iu = (J / 3) % 3, inpb = (J / 9) % 6, itkb = J / 54;
     constexpr int TKB = 1 << itkb, NPB = 1 << inpb, U = 1 << iu, KG = 1 << ikg;
+    constexpr int RC = few ? kConv2FewCopies : kConv2MaxCopies;
     if constexpr (conv2_regs_ok(TKB, NPB, KG) && I % DS_NSLICES == DS_SLICE)
-        g_conv_mfma2[I] = reinterpret_cast<const void *>(&conv_mfma2<TKB, NPB, U, KG>);
+        g_conv_mfma2[I] = reinterpret_cast<const void *>(&conv_mfma2<TKB, NPB, U, KG, RC>);
 }
 
 template <size_t... I>
