@@ -88,20 +88,21 @@ def counters(db):
 
 
 def paired_reduce(cur, kname, threads, red):
-    """Durations of the reduce dispatches that directly follow (in start time)
-    a dispatch of kname at the given grid: the reduce launch of that split
-    schedule, not the same reduce kernel of other tasks.  Empty when the
-    trace has no start times."""
+    """(kernel, reduce) duration pairs of the dispatches of kname at the given
+    grid that are directly followed (in start time) by a dispatch of red: the
+    launches of that split schedule, not the same kernel instance or reduce of
+    another task that shares the grid.  Empty when the trace has no start
+    times."""
     cols = [c[0] for c in cur.execute("select * from kernels limit 1").description]
     if "start" not in cols:
         return []
     seq = list(cur.execute('select name, start, duration, grid_x * grid_y * grid_z from kernels '
                            'order by start'))
     out = []
-    for (name, _, _, g), nxt in zip(seq, seq[1:]):
+    for (name, _, d, g), nxt in zip(seq, seq[1:]):
         if short(name) == kname and (threads is None or g == threads) and short(nxt[0]) == red:
-            out.append(nxt[2])
-    return sorted(out)
+            out.append((d, nxt[2]))
+    return out
 
 
 def bench_check(db, bench_json):
@@ -117,7 +118,14 @@ def bench_check(db, bench_json):
     cur = sqlite3.connect(db).cursor()
     rows = list(cur.execute("select name, duration, grid_x * grid_y * grid_z from kernels"))
     durs = [(d, g) for name, d, g in rows if short(name) == kname]
-    at = sorted(d for d, g in durs if threads is None or g == threads)
+    pairs = paired_reduce(cur, kname, threads, red) if red else []
+    if pairs:
+        # a split schedule: its own launches are the ones its reduce follows
+        at = sorted(d for d, _ in pairs)
+        what_k = "this instance, this grid, followed by the reduce"
+    else:
+        at = sorted(d for d, g in durs if threads is None or g == threads)
+        what_k = "this instance, this grid"
     print(f"\n### Dominant kernel of the profiled bench.py run\n")
     what = f"`{kname}`" + (f" followed by `{red}`" if red else "")
     print(f"bench.py: {what} on task {rf['task']}, average launch {rf['avg_launch_us']:.3f} us "
@@ -128,12 +136,12 @@ def bench_check(db, bench_json):
         return
     mean = sum(at) / len(at) / 1e3
     med = at[len(at) // 2] / 1e3
-    print("| kernel | dispatches (this instance, this grid) | mean us | median us | min us |")
+    print(f"| kernel | dispatches ({what_k}) | mean us | median us | min us |")
     print("|---|---:|---:|---:|---:|")
     print(f"| `{kname}` | {len(at)} of {len(durs)} | {mean:.3f} | {med:.3f} | {at[0] / 1e3:.3f} |")
     total = med
     if red:
-        rd, how = paired_reduce(cur, kname, threads, red), "after each of them"
+        rd, how = sorted(r for _, r in pairs), "after each of them"
         if not rd:
             # no dispatch times in the trace: every reduce of that grid
             rd = sorted(d for name, d, g in rows if short(name) == red and (rgrid is None or g == rgrid))

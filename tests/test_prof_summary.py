@@ -1,6 +1,7 @@
 """Host logic of the profile summaries (no GPU): kernel-name shortening and the
 pairing of a split schedule's conv dispatches with the reduce launch that
-follows each of them in a kernel trace."""
+follows each of them in a kernel trace (dispatches of the same instance and
+grid that no reduce follows belong to another task)."""
 import sqlite3
 
 from paper_2406_20037_amd import prof_summary as ps
@@ -35,11 +36,13 @@ def test_reduce_paired_with_the_dispatch_before_it():
             (OTHER, 650, 500, 802816), (RED, 1200, 100, 1048576),   # another task's reduce
             (CONV, 2000, 595, 819200), (RED, 2600, 45, 1048576),
             (CONV, 3000, 597, 409600), (RED, 3600, 70, 1048576)]    # other grid
+    rows += [(CONV, 4000, 70, 819200), (OTHER, 4100, 500, 802816)]   # same grid, no reduce
     cur = trace(rows)
-    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == [40, 45]
+    want = [(590, 40), (595, 45)]
+    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == want
     # rows inserted out of time order pair the same way
     cur = trace(list(reversed(rows)))
-    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == [40, 45]
+    assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == want
 
 
 def test_no_start_times_gives_no_pairs():
