@@ -1022,8 +1022,7 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG, RC)) void co
     issue(ci0, 0);
 
     // lane bases (floats) inside a buffer
-    int bb[NPB], oq[NPB];
-    bool pv[NPB];
+    int bb[NPB];
     const int shift = a.hal ? col0 & 3 : 0;
 #pragma unroll
     for (int b = 0; b < NPB; ++b) {
@@ -1034,15 +1033,11 @@ __global__ __launch_bounds__(256 * KG, conv2_waves(TKB, NPB, U, KG, RC)) void co
             const int fc = min(f, a.F - 1);
             const int r = fdv(fc, a.f_q), q = fc - r * a.Q;
             const int img = fdv(r, a.f_p), p = r - img * a.P;
-            pv[b] = f < a.F;
             bb[b] = a.bufw + lg * a.cs + ((img - n0) * a.hp + p * a.st - g0) * a.ws + q * a.st + shift;
-            oq[b] = img * a.K * PQ + p * a.Q + q;
         } else {
+            // pixels past the output read in-buffer operands (discarded)
             const int py = pix >> a.ltw, px = pix & (a.tw - 1);
-            const int p = pt * a.th + py, q = qt * a.tw + px;
-            pv[b] = pix < a.npx && p < a.P && q < a.Q;
             bb[b] = a.bufw + lg * a.cs + py * a.st * a.ws + px * a.st + shift;
-            oq[b] = p * a.Q + q;
         }
     }
     const int ab = li * a.wrow + lg * RS;
