@@ -795,10 +795,10 @@ __device__ __forceinline__ void copy(const char *base, unsigned off, float *dst)
 }  // namespace q4
 
 // Waves per SIMD each conv_mfma2 instance is compiled to allow: the most of
-// 6, 5, 4, 3 and 2 for which its registers fit without spilling (found by
-// compiling every instance under each bound), separately for the instances
-// that hold 12 copy units per thread in registers and those that hold 4;
-// others keep the compiler's choice.  On its own the compiler keeps the
+// 4, 3 and 2 (instances that hold 12 copy units per thread in registers) or
+// of 6, 5, 4, 3 and 2 (those that hold 4) for which its registers fit without
+// spilling, found by compiling every instance under each bound; others keep
+// the compiler's choice.  On its own the compiler keeps the
 // accumulators in AGPRs beside the VGPRs and ends at fewer waves:
 // conv_mfma2<4, 4, 1, 1, 12>, for one, takes 164 VGPRs + 64 AGPRs (2 waves)
 // unbounded and 152 VGPRs (3 waves) bounded; with 4 copy units, 119 VGPRs (4

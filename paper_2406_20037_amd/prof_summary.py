@@ -15,6 +15,7 @@ import collections
 import hashlib
 import json
 import os
+import re
 import sqlite3
 import sys
 
@@ -27,15 +28,26 @@ KERNEL_SOURCES = {
 }
 
 
+_COMMENT = re.compile(r"/\*.*?\*/|//[^\n]*", re.S)
+
+
+def code_digest(paths) -> str:
+    """sha256 over the code of the given source files: comments removed and
+    whitespace runs collapsed, so an edit to a comment keeps the digest."""
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, encoding="utf-8") as fh:
+            text = _COMMENT.sub(" ", fh.read())
+        h.update(" ".join(text.split()).encode())
+        h.update(b"\0")
+    return h.hexdigest()
+
+
 def source_hash(kernel: str) -> str | None:
-    """sha256 over the source files a kernel family is compiled from."""
+    """Code digest of the source files a kernel family is compiled from."""
     for prefix, files in KERNEL_SOURCES.items():
         if kernel.startswith(prefix):
-            h = hashlib.sha256()
-            for f in files:
-                with open(os.path.join(PKG, f), "rb") as fh:
-                    h.update(fh.read())
-            return h.hexdigest()
+            return code_digest(os.path.join(PKG, f) for f in files)
     return None
 
 

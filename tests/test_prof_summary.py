@@ -48,3 +48,17 @@ def test_reduce_paired_with_the_dispatch_before_it():
 def test_no_start_times_gives_no_pairs():
     cur = trace([(CONV, 0, 590, 819200), (RED, 600, 40, 1048576)], with_start=False)
     assert ps.paired_reduce(cur, "conv_mfma2<2, 8, 2, 1>", 819200, "split_reduce_kernel<8>") == []
+
+
+def test_code_digest_ignores_comments_not_code(tmp_path):
+    a = tmp_path / "a.hip"
+    a.write_text("// header\nint f(int x) {\n    return x + 1;   /* one */\n}\n")
+    d0 = ps.code_digest([a])
+    a.write_text("// header, reworded\n/* a block\n   comment */\nint f(int x) {\n  return x + 1;\n}\n")
+    assert ps.code_digest([a]) == d0
+    a.write_text("int f(int x) {\n    return x + 2;\n}\n")
+    assert ps.code_digest([a]) != d0
+    # file boundaries count: the same files in another order are another digest
+    b = tmp_path / "b.hip"
+    b.write_text("")
+    assert ps.code_digest([a, b]) != ps.code_digest([b, a])
