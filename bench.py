@@ -247,8 +247,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus}): this build tunes and "
-              "times kernels on a single device and has no multi-GPU mode.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for {args.gpus}): the tuner and the timed "
+              "passes run on a single device; there is no multi-GPU mode.", file=sys.stderr)
         return 2
 
     import torch
