@@ -217,6 +217,39 @@ def test_parity_misaligned_operands(torch_dev, lib, shift_x, shift_w):
             assert np.array_equal(out, ref), f"{sh} shift x {shift_x} w {shift_w} {o.knobs(p)}"
 
 
+@pytest.mark.parametrize("mfma,th,tw", [(2, 16, 16), (3, 8, 16)], ids=["rect_4x4", "band_4x2"])
+def test_register_budget_follows_copy_width(torch_dev, lib, mfma, th, tw):
+    """A point whose 16-byte copies need at most 4 units per thread runs the
+    channel-quad build that holds 4 copy sources in registers; on operands 4
+    bytes past a 16-byte boundary the same point copies 4 bytes at a time,
+    needs more units and runs the 12-unit build.  Eight chunks per workgroup,
+    so the held sources are reused; both runs match the oracle exactly."""
+    torch = torch_dev
+    sh = (2, 32, 28, 28, 64, 3, 3, 1, 1)
+    kn = dict(tk=64, th=th, tw=tw, tc=4, unroll=0, lds=1, ks=1, mfma=mfma, vec=4)
+    space = lib.Space(1, sh)
+    s16, s4 = space.sched_of(**kn), space.sched_of(**dict(kn, vec=1))
+    assert space.valid(s16.index()) and space.valid(s4.index())
+    assert space.kernel_info(s16.index())["params"][4] == 4
+    assert space.kernel_info(s4.index())["params"][4] == 12
+    x, w = synthdata.conv_inputs(sh, "int")
+    ref = ok.conv2d_f64(x, w, sh).ravel()
+    y = torch.empty(ref.size, dtype=torch.float32, device="cuda:0")
+    def shifted(a, k):
+        buf = torch.zeros(a.size + k, dtype=torch.float32, device="cuda:0")
+        buf[k:] = torch.from_numpy(np.ascontiguousarray(a).ravel()).to("cuda:0")
+        return buf[k:]
+
+    for shift in (0, 1):
+        xd, wd = shifted(x, shift), shifted(w, shift)
+        assert (xd.data_ptr() % 16 == 0) == (wd.data_ptr() % 16 == 0) == (shift == 0)
+        print("register budget", mfma, th, tw, "shift", shift, flush=True)
+        y.fill_(float("nan"))
+        lib.kernel_run(1, s16, xd, wd, y)
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy().astype(np.float64), ref), f"shift {shift}"
+
+
 BAND_CASES = [
     ("band_14_cross", (2, 16, 14, 14, 32, 3, 3, 1, 1)),
     ("band_7_multi", (3, 8, 7, 7, 16, 3, 3, 1, 1)),
