@@ -60,7 +60,9 @@ def traffic_key(kernel: str, sched: str, shape=None) -> str:
     same instance runs with different runtime tile arguments).  The unroll knob
     and the instance's unroll factor are left out: they order instructions and
     set how far ahead operands are read, but never change the addresses a
-    launch reads or writes.  The problem shape, when given, ends the key."""
+    launch reads or writes.  Band tiles (conv mfma 3) are th * tw consecutive
+    output pixels, so their th and tw enter only as that product (npx).  The
+    problem shape, when given, ends the key."""
     name = kernel
     if "<" in kernel and kernel.endswith(">"):
         fam, args = kernel[:-1].split("<", 1)
@@ -70,6 +72,11 @@ def traffic_key(kernel: str, sched: str, shape=None) -> str:
             parts[pos] = "*"
         name = f"{fam}<{', '.join(parts)}>"
     kept = [kv for kv in sched.split(",") if kv and not kv.startswith("unroll=")]
+    kv = dict(k.split("=", 1) for k in kept)
+    if kv.get("mfma") == "3" and "th" in kv and "tw" in kv:
+        npx = int(kv["th"]) * int(kv["tw"])
+        kept = [k for k in kept if not k.startswith(("th=", "tw="))]
+        kept.insert(1 if kept and kept[0].startswith("tk=") else 0, f"npx={npx}")
     key = f"{name} {','.join(kept)}" if kept else name
     if shape:
         key += " shape=" + ",".join(str(int(v)) for v in shape)

@@ -62,3 +62,18 @@ def test_code_digest_ignores_comments_not_code(tmp_path):
     b = tmp_path / "b.hip"
     b.write_text("")
     assert ps.code_digest([a, b]) != ps.code_digest([b, a])
+
+
+def test_traffic_key_band_tiles_by_pixel_count():
+    sh = (16, 256, 56, 56, 256, 3, 3, 1, 1)
+    a = ps.traffic_key("conv_mfma2<4, 4, 1, 1, 4>",
+                       "tk=64,th=64,tw=4,tc=4,unroll=16,lds=1,ks=4,mfma=3,vec=4", sh)
+    b = ps.traffic_key("conv_mfma2<4, 4, 1, 1, 4>",
+                       "tk=64,th=8,tw=32,tc=4,unroll=0,lds=1,ks=4,mfma=3,vec=4", sh)
+    assert a == b and "npx=256" in a and "th=" not in a and "*" in a
+    # rectangular tiles keep th and tw: the same product is another tile
+    c = ps.traffic_key("conv_mfma2<4, 4, 1, 1, 4>",
+                       "tk=64,th=8,tw=32,tc=4,unroll=0,lds=1,ks=1,mfma=2,vec=4", sh)
+    d = ps.traffic_key("conv_mfma2<4, 4, 1, 1, 4>",
+                       "tk=64,th=16,tw=16,tc=4,unroll=0,lds=1,ks=1,mfma=2,vec=4", sh)
+    assert c != d and "th=8,tw=32" in c
