@@ -330,8 +330,7 @@ def conv_quad_geometry(shape, v):
     consecutive input channels) at one tap (r, s), over LDS-staged weights and
     input halo.  Waves split the tile's pixels as for mfma = 1 (16x16 blocks,
     up to four pixel waves); the unroll knob gives the depth D (3 from 16
-    unrolled steps, 2 from 4, else 1, lowered until U = 2^(D-1) divides the
-    chunk's quads) and a step takes U quads.  A
+    unrolled steps, 2 from 4, else 1) and a step takes U = 2^(D-1) quads.  A
     reduction split ks first goes to KG wave groups of one workgroup (the
     largest of 4, 2, 1 not above ks whose U-blocks of quads divide the chunk's
     quads and that keeps 1024 threads), the rest across workgroups.
@@ -371,11 +370,9 @@ def conv_quad_geometry(shape, v):
     blocks = tkb * npb
     uf = 1 if v["unroll"] == 0 else min(16, _pow2floor(max(1, v["unroll"] // blocks)))
     depth = 3 if uf >= 16 else (2 if uf >= 4 else 1)
+    quads_per_step = 2 ** (depth - 1)
     chan = C if C < 4 else tc                  # real channels of a full chunk
     quads = _cdiv(chan, 4)
-    while depth > 1 and quads % 2 ** (depth - 1):
-        depth -= 1                             # capped to what a chunk holds
-    quads_per_step = 2 ** (depth - 1)
     ok = tk >= 16 and npx >= 16 and (tc >= 4 or (C < 4 and tc == 1))
     ok = ok and (band or (th <= P and tw <= Q))
     kg = min(v["ks"], 4)

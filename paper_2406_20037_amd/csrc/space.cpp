@@ -93,12 +93,7 @@ Geometry conv_geometry(const int64_t *sh, const int32_t *v) {
         // blocks
         const int body2 = std::max(1, tk / 16) * std::max(1, npx / (16 * std::min(4, std::max(1, npx / 16))));
         const int ue = unroll == 0 ? 1 : std::min(16, pow2_floor(std::max(1, unroll / body2)));
-        int depth = ue >= 16 ? 3 : (ue >= 4 ? 2 : 1);
-        // the quads one loop step multiplies divide a chunk's quads: a depth
-        // the chunk cannot hold is capped (the same program as the lower
-        // unroll values, like a saturated unroll)
-        const int64_t quads = ((C < 4 ? C : tc) + 3) / 4;
-        while (depth > 1 && quads % (int64_t(1) << (depth - 1)) != 0) --depth;
+        const int depth = ue >= 16 ? 3 : (ue >= 4 ? 2 : 1);
         Conv2Args a;
         const Conv2Shape c = conv2_setup(sh, tk, th, tw, tc, depth, ks, vec, mfma == 3, a);
         g.threads = c.threads;

@@ -217,19 +217,10 @@ def test_conv_quad_geometry_hand_computed():
     # groups of four waves, 64 * 4 * 4 = 1024 threads
     g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=64, unroll=0, lds=1, ks=4, mfma=2, vec=4))
     assert g["valid"] and g["threads"] == 1024 and g["grid"] == 224
-    # 8-channel chunks hold 2 quads: unroll 64 over one block asks for depth 3
-    # (4 quads per step), which they cannot hold; the depth is capped at 2 (2
-    # quads per step), the same program as unroll 16 and 512.  With one quad
-    # per step and ks = 4 the groups fall back to two (2 % 4 != 0), the
-    # remaining factor 2 splits across workgroups
-    g64 = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=8, unroll=64, lds=1, ks=1, mfma=2, vec=4))
-    assert g64["valid"] and g64["unroll_eff"] == 2
-    for u in (16, 512):
-        assert s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=8, unroll=u, lds=1, ks=1, mfma=2,
-                                 vec=4)) == g64
-    # one-quad chunks (tc = 4) keep one quad per step whatever the unroll
-    g4 = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=4, unroll=512, lds=1, ks=1, mfma=2, vec=4))
-    assert g4["valid"] and g4["unroll_eff"] == 1
+    # 8-channel chunks hold 2 quads: unroll 64 (4 quads per step) does not fit
+    # them; with one quad per step and ks = 4 the groups fall back to two
+    # (2 % 4 != 0), the remaining factor 2 splits across workgroups
+    assert not s.valid(idx_of(s, tk=16, th=4, tw=16, tc=8, unroll=64, lds=1, ks=1, mfma=2, vec=4))
     g = s.geometry(idx_of(s, tk=16, th=4, tw=16, tc=8, unroll=0, lds=1, ks=4, mfma=2, vec=4))
     assert g["valid"] and g["threads"] == 512 and g["grid"] == 2 * 224 and g["chunks"] == 8
     # chunks of whole quads: tc = 2 on 64 channels is not; LDS staging only
