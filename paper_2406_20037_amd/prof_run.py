@@ -64,6 +64,8 @@ def main(argv=None):
     knobs = {k: int(v) for k, v in (kv.split("=") for kv in args.sched.split(","))}
     space = L.Space(op, shape)
     s = space.sched_of(**knobs)
+    if not space.valid(s.index()):
+        ap.error(f"{args.sched} is not a valid point of {args.workload}'s space")
     if op == wl.OP_CONV:
         x, w = synthdata.conv_inputs(shape, kind)
         N, C, H, W, K, R, S, st, pd = shape
@@ -87,7 +89,10 @@ def main(argv=None):
         # twice (warm-up and timed repeat)
         cfg = L.measure_cfg(warmup=1, repeat=1, min_repeat_ms=1e9, max_number=args.iters,
                             check=0, graph=1)
-        L.ds_measure(s, L.make_io(xd, wd, yd, None, torch.cuda.current_stream()), cfg)
+        m = L.ds_measure(s, L.make_io(xd, wd, yd, None, torch.cuda.current_stream()), cfg)
+        if m.status != L.DS_OK:
+            raise SystemExit(f"measurement of {args.sched} failed: "
+                             f"{L.STATUS_NAMES.get(m.status, m.status)}")
     n = args.copy_mib * (1 << 20) // 4
     a = torch.ones(n, device="cuda:0")
     b = torch.empty_like(a)
