@@ -57,7 +57,10 @@ geometry of named points are checked in tests/test_oracle_space.py.  The
 validity half (register, LDS and thread budgets) is pinned against the
 compiled kernels on the GPU (tests/test_gpu_instances.py): every instance a
 valid point of the five workloads can select launches bit-exact, spills
-nothing, and fits its launch bound and LDS.
+nothing, and fits its launch bound and LDS.  The paper prints no launch
+geometry (grid, threads, LDS bytes, accumulators), so against the paper that
+half is parity unpinned; its pins are the hand-computed points and the
+compiled kernels above.
 """
 from __future__ import annotations
 
