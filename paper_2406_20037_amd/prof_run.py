@@ -23,7 +23,8 @@ sys.path.insert(0, ROOT)
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="matmul_1024",
-                    help="a single-kernel workload or a network layer (resnet50:NAME, vgg16:NAME)")
+                    help="a single-kernel workload, a network layer (resnet50:NAME, vgg16:NAME) "
+                         "or a conv shape (conv:N,C,H,W,K,R,S,stride,pad; He-normal inputs)")
     ap.add_argument("--sched", help="knob=value,... (every axis)")
     ap.add_argument("--mfma-ceiling", action="store_true",
                     help="launch the library's pure-MFMA calibration kernel --iters times "
@@ -53,7 +54,10 @@ def main(argv=None):
         return 0
     if not args.sched:
         ap.error("--sched is required unless --mfma-ceiling")
-    if ":" in args.workload:          # a network layer, e.g. vgg16:L6_256_256_56
+    if args.workload.startswith("conv:"):   # any conv shape: conv:N,C,H,W,K,R,S,stride,pad
+        op, shape = wl.OP_CONV, tuple(int(v) for v in args.workload[5:].split(","))
+        kind = "he"
+    elif ":" in args.workload:        # a network layer, e.g. vgg16:L6_256_256_56
         net, layer = args.workload.split(":", 1)
         table = {"resnet50": wl.RESNET50, "vgg16": wl.VGG16}[net]
         op, shape = next((o, sh) for name, o, sh, _ in table if name == layer)

@@ -19,6 +19,8 @@ OURS = re.compile(r"^\| `(conv_valu|conv_mfma2?|mm_valu|mm_mfma|split_reduce_ker
 
 
 def resolve(workload):
+    if workload.startswith("conv:"):
+        return wl.OP_CONV, tuple(int(v) for v in workload[5:].split(","))
     if ":" in workload:
         net, layer = workload.split(":", 1)
         table = {"resnet50": wl.RESNET50, "vgg16": wl.VGG16}[net]
